@@ -1,0 +1,151 @@
+/*
+ * treewy.h - C ABI of libtreewy.so: tree-structured WY verification of the
+ * gated delta rule on AMD Instinct MI355X (gfx950).
+ *
+ * Notation (paper: Background, eq. 1; Method, eq. 2 and eq. 3).  For every
+ * sequence b and value head h ("unit") there is a committed recurrent state
+ * S0 in R^{d_v x d_k}.  A draft tree of N nodes is given by parent pointers
+ * with parent[t] in [-1, t-1] (-1 = the node hangs directly off S0), so that
+ * every ancestor of t has a smaller index.  Node t carries q_t, k_t in R^{d_k},
+ * v_t in R^{d_v}, a decay gate alpha_t and a write strength beta_t.  The gated
+ * delta rule S_t = alpha_t S_p (I - beta_t k_t k_t^T) + beta_t v_t k_t^T,
+ * o_t = S_t q_t (eq. 1) applied along every root-to-node path defines what
+ * these calls compute.
+ *
+ * Conventions shared by every call:
+ *  - All tensor pointers are DEVICE pointers to row-major, contiguous arrays
+ *    whose base address is 16-byte aligned.  The caller allocates and owns
+ *    every buffer; the library allocates nothing and keeps no state between
+ *    calls, so calls are re-entrant.
+ *  - Sizes supported: d_k == d_v == 128, 0 <= N <= 64 (N = 0 is an empty
+ *    draft), 0 <= L_max <= 64, B * H < 2^31; other sizes return
+ *    TREEWY_ERR_UNSUPPORTED, negative sizes TREEWY_ERR_INVALID_ARG.  B == 0 or
+ *    H == 0 launches nothing and returns TREEWY_OK; so does N == 0 for the
+ *    verify calls (commit with N == 0 still copies S0 to S_new).
+ *  - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
+ *    stream) and returns after the launch.  The returned status covers only
+ *    what the host can check without reading device memory; a failed launch
+ *    returns TREEWY_ERR_HIP.
+ *  - Malformed trees or paths are found on the device: when `err` (device
+ *    int32 [B], nullable) is given, the kernels OR a TREEWY_FLAG_* bit into
+ *    err[b] and never read or write out of bounds.  The caller zeroes err.
+ *  - All heads of a sequence share its tree (parent[b]) and its path.
+ *  - alpha must lie in (0, 1] and beta in [0, 1] (the paper's gates lie in
+ *    (0, 1)); other values are not checked.
+ */
+#ifndef TREEWY_H
+#define TREEWY_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum treewy_status {
+    TREEWY_OK = 0,
+    TREEWY_ERR_INVALID_ARG = 1,  /* null or misaligned pointer, negative size, bad dtype */
+    TREEWY_ERR_UNSUPPORTED = 2,  /* d_k or d_v != 128, N or L_max above 64, too many units */
+    TREEWY_ERR_HIP = 3           /* the HIP runtime refused the launch */
+} treewy_status;
+
+typedef enum treewy_dtype {
+    TREEWY_F32 = 0,              /* q, k, v and o in float32 */
+    TREEWY_BF16 = 1              /* q, k, v and o in bfloat16 (state, U, alpha, beta stay float32) */
+} treewy_dtype;
+
+#define TREEWY_FLAG_BAD_PARENT 1 /* some parent[b][t] outside [-1, t-1]; treated as -1 */
+#define TREEWY_FLAG_BAD_PATH 2   /* path[b] is not a root-to-node path; state left unchanged */
+
+/*
+ * treewy_verify - one triangular solve for the whole draft (Method, eq. 2).
+ *
+ * Forms, per unit, the ancestor-masked, decay-weighted system
+ *   (I + diag(beta) G) U = R,  G[t,i] = (g_t/g_i) (k_t . k_i) [i strict ancestor of t],
+ *   R[t] = beta_t v_t - beta_t g_t (S0 k_t),
+ * where g_t is the product of alpha over t and its ancestors, solves it for the
+ * pseudo-values U (the paper's V-tilde, N x d_v), and reads every node's output
+ *   o_t = g_t S0 q_t + sum over i ancestor-or-self of t of (g_t/g_i) (k_i . q_t) U[i]
+ * out of the same solve (equal to S_t q_t of eq. 1).
+ *
+ *   S0     [B, H, d_v, d_k] float32        committed states (read only)
+ *   q, k   [B, H, N, d_k]   in_dtype
+ *   v      [B, H, N, d_v]   in_dtype
+ *   alpha, beta [B, H, N]   float32
+ *   parent [B, N]           int32          parent[b][t] in [-1, t-1]
+ *   o      [B, H, N, d_v]   in_dtype       written: every node's output
+ *   U      [B, H, N, d_v]   float32        written: pseudo-values, read by treewy_commit
+ *   err    [B] int32 or NULL               TREEWY_FLAG_BAD_PARENT
+ */
+treewy_status treewy_verify(const float *S0, const void *q, const void *k, const void *v,
+                            const float *alpha, const float *beta, const int32_t *parent, int N,
+                            int B, int H, int d_k, int d_v, treewy_dtype in_dtype,
+                            void *o, float *U, int32_t *err, void *stream);
+
+/*
+ * treewy_commit - reconstruct only the accepted node's state (Method, eq. 3):
+ *   S_a = g_a S0 + sum over i on the root-to-a path of (g_a/g_i) U[i] k_i^T,
+ * which becomes the next round's S0.  Replaces full-state snapshotting.
+ *
+ *   S0       [B, H, d_v, d_k] float32      committed states
+ *   U        [B, H, N, d_v]   float32      pseudo-values from treewy_verify
+ *   k        [B, H, N, d_k]   k_dtype      the keys given to treewy_verify
+ *   alpha    [B, H, N]        float32
+ *   path     [B, L_max]       int32        root -> accepted node; entries past path_len ignored
+ *   path_len [B]              int32        0 = nothing accepted: S_new = S0 bit for bit
+ *   parent   [B, N] int32 or NULL          when given, each path is checked against the tree
+ *   S_new    [B, H, d_v, d_k] float32      written; may be the same buffer as S0 (in place)
+ *   err      [B] int32 or NULL             TREEWY_FLAG_BAD_PATH (that sequence keeps S0)
+ * Without `parent` a path is only checked to be strictly increasing and in [0, N).
+ */
+treewy_status treewy_commit(const float *S0, const float *U, const void *k, const float *alpha,
+                            const int32_t *path, const int32_t *path_len, int L_max,
+                            const int32_t *parent, int N, int B, int H, int d_k, int d_v,
+                            treewy_dtype k_dtype, float *S_new, int32_t *err, void *stream);
+
+/*
+ * treewy_snapshot_verify - full-state-snapshotting baseline (Section "The
+ * memory problem", approach (i)): runs eq. 1 node by node and writes every
+ * node's full state, so that commit is a copy of one snapshot.  Same inputs
+ * and outputs as treewy_verify except:
+ *   snapshots [B, H, N, d_v, d_k] float32  written: S_t of every node
+ * The speculative memory is N full states per unit instead of U.
+ */
+treewy_status treewy_snapshot_verify(const float *S0, const void *q, const void *k, const void *v,
+                                     const float *alpha, const float *beta, const int32_t *parent,
+                                     int N, int B, int H, int d_k, int d_v, treewy_dtype in_dtype,
+                                     void *o, float *snapshots, int32_t *err, void *stream);
+
+/*
+ * treewy_snapshot_commit - rollback by indexing (approach (i)):
+ *   S_new[b,h] = snapshots[b,h,accepted[b]], or S0[b,h] when accepted[b] == -1.
+ *   accepted [B] int32 in [-1, N-1]; other values set TREEWY_FLAG_BAD_PATH and keep S0.
+ *   S_new may be the same buffer as S0.
+ */
+treewy_status treewy_snapshot_commit(const float *S0, const float *snapshots, const int32_t *accepted,
+                                     int N, int B, int H, int d_k, int d_v, float *S_new,
+                                     int32_t *err, void *stream);
+
+/*
+ * treewy_path_from_node - the root-to-node path of each sequence's accepted
+ * node, in the layout treewy_commit reads (Method: the accepted node's
+ * ancestors and itself).  Bit exact.
+ *   parent   [B, N] int32
+ *   accepted [B] int32 in [-1, N-1] (-1 = nothing accepted -> path_len 0)
+ *   path     [B, L_max] int32 written (root first; entries past the length set to -1)
+ *   path_len [B] int32 written
+ * A path longer than L_max, an out-of-range node or a malformed tree sets
+ * TREEWY_FLAG_BAD_PATH and path_len[b] = 0.
+ */
+treewy_status treewy_path_from_node(const int32_t *parent, const int32_t *accepted, int N, int B,
+                                    int L_max, int32_t *path, int32_t *path_len, int32_t *err,
+                                    void *stream);
+
+/* Static description of a status code; never NULL. */
+const char *treewy_status_string(treewy_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TREEWY_H */

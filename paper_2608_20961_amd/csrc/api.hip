@@ -1,0 +1,114 @@
+// C ABI of libtreewy.so: host-side argument checks, then one kernel launch on
+// the caller's stream.  Declared in include/treewy.h.
+#include <stdint.h>
+
+#include "device.h"
+#include "launch.h"
+
+namespace {
+
+constexpr int kMaxN = 64;
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+treewy_status hip_status(hipError_t e) { return e == hipSuccess ? TREEWY_OK : TREEWY_ERR_HIP; }
+
+// Shared checks for the calls that take the full verify inputs.
+treewy_status check_common(int N, int B, int H, int d_k, int d_v, treewy_dtype dt) {
+    if (B < 0 || H < 0 || N < 0) return TREEWY_ERR_INVALID_ARG;
+    if (dt != TREEWY_F32 && dt != TREEWY_BF16) return TREEWY_ERR_INVALID_ARG;
+    if (d_k != treewy::D || d_v != treewy::D) return TREEWY_ERR_UNSUPPORTED;
+    if (N > kMaxN) return TREEWY_ERR_UNSUPPORTED;
+    if ((int64_t)B * H > INT32_MAX) return TREEWY_ERR_UNSUPPORTED;
+    return TREEWY_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+treewy_status treewy_verify(const float *S0, const void *q, const void *k, const void *v,
+                            const float *alpha, const float *beta, const int32_t *parent, int N,
+                            int B, int H, int d_k, int d_v, treewy_dtype in_dtype, void *o, float *U,
+                            int32_t *err, void *stream) {
+    treewy_status st = check_common(N, B, H, d_k, d_v, in_dtype);
+    if (st != TREEWY_OK) return st;
+    if (N == 0 || B == 0 || H == 0) return TREEWY_OK;
+    if (!S0 || !q || !k || !v || !alpha || !beta || !parent || !o || !U) return TREEWY_ERR_INVALID_ARG;
+    if (!aligned16(S0) || !aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) ||
+        !aligned16(U))
+        return TREEWY_ERR_INVALID_ARG;
+    return hip_status(treewy::launch_verify(S0, q, k, v, alpha, beta, parent, N, B, H,
+                                            in_dtype == TREEWY_F32, o, U, err,
+                                            static_cast<hipStream_t>(stream)));
+}
+
+treewy_status treewy_commit(const float *S0, const float *U, const void *k, const float *alpha,
+                            const int32_t *path, const int32_t *path_len, int L_max,
+                            const int32_t *parent, int N, int B, int H, int d_k, int d_v,
+                            treewy_dtype k_dtype, float *S_new, int32_t *err, void *stream) {
+    treewy_status st = check_common(N, B, H, d_k, d_v, k_dtype);
+    if (st != TREEWY_OK) return st;
+    if (L_max < 0) return TREEWY_ERR_INVALID_ARG;
+    if (L_max > kMaxN) return TREEWY_ERR_UNSUPPORTED;
+    if (B == 0 || H == 0) return TREEWY_OK;
+    if (!S0 || !path_len || !S_new) return TREEWY_ERR_INVALID_ARG;
+    if (N > 0 && (!U || !k || !alpha)) return TREEWY_ERR_INVALID_ARG;
+    if (L_max > 0 && !path) return TREEWY_ERR_INVALID_ARG;
+    if (!aligned16(S0) || !aligned16(S_new)) return TREEWY_ERR_INVALID_ARG;
+    return hip_status(treewy::launch_commit(S0, U, k, alpha, path, path_len, L_max, parent, N, B, H,
+                                            k_dtype == TREEWY_F32, S_new, err,
+                                            static_cast<hipStream_t>(stream)));
+}
+
+treewy_status treewy_snapshot_verify(const float *S0, const void *q, const void *k, const void *v,
+                                     const float *alpha, const float *beta, const int32_t *parent,
+                                     int N, int B, int H, int d_k, int d_v, treewy_dtype in_dtype,
+                                     void *o, float *snapshots, int32_t *err, void *stream) {
+    treewy_status st = check_common(N, B, H, d_k, d_v, in_dtype);
+    if (st != TREEWY_OK) return st;
+    if (N == 0 || B == 0 || H == 0) return TREEWY_OK;
+    if (!S0 || !q || !k || !v || !alpha || !beta || !parent || !o || !snapshots)
+        return TREEWY_ERR_INVALID_ARG;
+    if (!aligned16(S0) || !aligned16(snapshots)) return TREEWY_ERR_INVALID_ARG;
+    return hip_status(treewy::launch_snapshot_verify(S0, q, k, v, alpha, beta, parent, N, B, H,
+                                                     in_dtype == TREEWY_F32, o, snapshots, err,
+                                                     static_cast<hipStream_t>(stream)));
+}
+
+treewy_status treewy_snapshot_commit(const float *S0, const float *snapshots, const int32_t *accepted,
+                                     int N, int B, int H, int d_k, int d_v, float *S_new,
+                                     int32_t *err, void *stream) {
+    treewy_status st = check_common(N, B, H, d_k, d_v, TREEWY_F32);
+    if (st != TREEWY_OK) return st;
+    if (B == 0 || H == 0) return TREEWY_OK;
+    if (!S0 || !accepted || !S_new || (N > 0 && !snapshots)) return TREEWY_ERR_INVALID_ARG;
+    if (!aligned16(S0) || !aligned16(S_new) || (snapshots && !aligned16(snapshots)))
+        return TREEWY_ERR_INVALID_ARG;
+    return hip_status(treewy::launch_snapshot_commit(S0, snapshots, accepted, N, B, H, S_new, err,
+                                                     static_cast<hipStream_t>(stream)));
+}
+
+treewy_status treewy_path_from_node(const int32_t *parent, const int32_t *accepted, int N, int B,
+                                    int L_max, int32_t *path, int32_t *path_len, int32_t *err,
+                                    void *stream) {
+    if (N < 0 || B < 0 || L_max < 0) return TREEWY_ERR_INVALID_ARG;
+    if (N > kMaxN || L_max > kMaxN) return TREEWY_ERR_UNSUPPORTED;
+    if (B == 0) return TREEWY_OK;
+    if (!accepted || !path_len || (N > 0 && !parent) || (L_max > 0 && !path))
+        return TREEWY_ERR_INVALID_ARG;
+    return hip_status(treewy::launch_path_from_node(parent, accepted, N, B, L_max, path, path_len,
+                                                    err, static_cast<hipStream_t>(stream)));
+}
+
+const char *treewy_status_string(treewy_status status) {
+    switch (status) {
+    case TREEWY_OK: return "ok";
+    case TREEWY_ERR_INVALID_ARG: return "invalid argument (null or misaligned pointer, bad size or dtype)";
+    case TREEWY_ERR_UNSUPPORTED: return "unsupported size (d_k, d_v must be 128; N, L_max at most 64)";
+    case TREEWY_ERR_HIP: return "HIP launch failed";
+    }
+    return "unknown status";
+}
+
+}  // extern "C"

@@ -1,0 +1,104 @@
+// treewy_commit kernel: rebuild the accepted node's state from the pseudo-values
+// (Method, eq. 3):  S_a = g_a S0 + sum_{l} w_l U[path_l] k_{path_l}^T,
+// with g_a the product of alpha along the path and w_l = g_a / g_{path_l} the
+// product of alpha over the path nodes after path_l.
+//
+// One workgroup per (sequence, head) streams its 64 KiB state: every thread
+// owns sixteen float4s at stride 4 KiB, so each load and store instruction of
+// the workgroup covers 4 KiB of contiguous HBM.  The path's scaled pseudo-value
+// rows and keys (at most 64 x 128 each) are staged in LDS.  Each thread reads
+// and writes only its own elements, so S_new may alias S0.
+#include "device.h"
+#include "launch.h"
+
+namespace treewy {
+
+constexpr int MAX_PATH = 64;
+
+template <bool F32K>
+__global__ __launch_bounds__(THREADS) void commit_kernel(
+    const float *S0, const float *__restrict__ U, const void *__restrict__ k_,
+    const float *__restrict__ alpha, const int32_t *__restrict__ path,
+    const int32_t *__restrict__ path_len, int L_max, const int32_t *__restrict__ parent, int N,
+    int H, float *S_new, int32_t *__restrict__ err) {
+    using In = typename std::conditional<F32K, float, __bf16>::type;
+    extern __shared__ __attribute__((aligned(16))) float stage[];   // Uw [L_max][D], Kp [L_max][D]
+    __shared__ int s_node[MAX_PATH];
+    __shared__ float s_w[MAX_PATH];
+    __shared__ float s_w0;
+    __shared__ int s_len;
+
+    const In *k = static_cast<const In *>(k_);
+    const int tid = threadIdx.x, u = blockIdx.x, b = u / H;
+    const size_t node0 = (size_t)u * N;
+
+    const f32x4 *src = reinterpret_cast<const f32x4 *>(S0 + (size_t)u * D * D);
+    f32x4 s[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s[i] = src[tid + THREADS * i];
+
+    if (tid == 0) {
+        const int len = path_len[b];
+        bool ok = len >= 0 && len <= L_max;
+        int prev = -1;
+        for (int l = 0; ok && l < len; ++l) {
+            const int a = path[(size_t)b * L_max + l];
+            if (a < 0 || a >= N || a <= prev || (parent && parent[(size_t)b * N + a] != prev))
+                ok = false;
+            else
+                s_node[l] = a;
+            prev = a;
+        }
+        float w = 1.f;
+        if (ok)
+            for (int l = len - 1; l >= 0; --l) {
+                s_w[l] = w;
+                w *= alpha[node0 + s_node[l]];
+            }
+        s_len = ok ? len : 0;
+        s_w0 = ok ? w : 1.f;
+        if (!ok) flag_error(err, b, TREEWY_FLAG_BAD_PATH);
+    }
+    __syncthreads();
+    const int len = s_len;
+    float *Uw = stage;
+    float *Kp = stage + (size_t)L_max * D;
+    for (int idx = tid; idx < len * D; idx += THREADS) {
+        const int l = idx / D, c = idx % D;
+        const size_t row = (node0 + s_node[l]) * D + c;
+        Uw[idx] = s_w[l] * U[row];
+        Kp[idx] = to_f32(k[row]);
+    }
+    __syncthreads();
+
+    const float w0 = s_w0;
+    const int r0 = tid >> 5, c4 = (tid & 31) * 4;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s[i] *= w0;
+    for (int l = 0; l < len; ++l) {
+        const f32x4 kk = *reinterpret_cast<const f32x4 *>(Kp + l * D + c4);
+        const float *uw = Uw + l * D + r0;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) s[i] += uw[8 * i] * kk;
+    }
+    f32x4 *dst = reinterpret_cast<f32x4 *>(S_new + (size_t)u * D * D);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) dst[tid + THREADS * i] = s[i];
+}
+
+hipError_t launch_commit(const float *S0, const float *U, const void *k, const float *alpha,
+                         const int32_t *path, const int32_t *path_len, int L_max,
+                         const int32_t *parent, int N, int B, int H, bool f32_k, float *S_new,
+                         int32_t *err, hipStream_t stream) {
+    const dim3 grid((unsigned)(B * H)), block(THREADS);
+    const size_t lds = (size_t)2 * L_max * D * sizeof(float);
+    if (f32_k)
+        hipLaunchKernelGGL((commit_kernel<true>), grid, block, lds, stream, S0, U, k, alpha, path,
+                           path_len, L_max, parent, N, H, S_new, err);
+    else
+        hipLaunchKernelGGL((commit_kernel<false>), grid, block, lds, stream, S0, U, k, alpha, path,
+                           path_len, L_max, parent, N, H, S_new, err);
+    return hipGetLastError();
+}
+
+}  // namespace treewy

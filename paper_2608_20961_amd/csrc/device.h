@@ -1,0 +1,58 @@
+// Device helpers shared by the libtreewy kernels (gfx950 / CDNA4).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "treewy.h"
+
+namespace treewy {
+
+constexpr int D = 128;          // d_k == d_v
+constexpr int THREADS = 256;    // four wave64s per workgroup
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// D(32x32) += A(32x16) B(16x32) on the matrix cores, bf16 in, fp32 accumulate.
+// Lane l supplies row l%32 of A and column l%32 of B, each with the eight
+// contraction indices of group l/32; lane l receives column l%32 of D at rows
+// 8*(r/4) + 4*(l/32) + r%4 in accumulator element r.
+__device__ __forceinline__ f32x16 mma(bf16x8 a, bf16x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Row of the 32x32 accumulator tile held in element r by lanes of group hg.
+__device__ __forceinline__ int acc_row(int r, int hg) { return 8 * (r >> 2) + 4 * hg + (r & 3); }
+
+// fp32 -> bf16 pair with x ~= hi + lo (|x - hi - lo| <= 2^-16 |x|); both round to nearest even.
+__device__ __forceinline__ void split8(const float *x, bf16x8 &hi, bf16x8 &lo) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        __bf16 h = (__bf16)x[e];
+        hi[e] = h;
+        lo[e] = (__bf16)(x[e] - (float)h);
+    }
+}
+
+__device__ __forceinline__ bf16x8 round8(const float *x) {
+    bf16x8 h;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) h[e] = (__bf16)x[e];
+    return h;
+}
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(__bf16 x) { return (float)x; }
+
+template <typename T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ __bf16 from_f32<__bf16>(float x) { return (__bf16)x; }
+
+__device__ __forceinline__ void flag_error(int32_t *err, int b, int flag) {
+    if (err) atomicOr(err + b, flag);
+}
+
+}  // namespace treewy

@@ -81,11 +81,9 @@ WORKLOADS: Dict[int, Workload] = {
 def scaled(w: Workload, B: Optional[int] = None, H: Optional[int] = None,
            N: Optional[int] = None) -> Workload:
     """Same distributions, different sizes (used for small parity cases)."""
-    return dataclasses.replace(w, B=B if B is not None else w.B,
-                               H=H if H is not None else w.H,
-                               N=N if N is not None else w.N,
-                               max_depth=min(w.max_depth, N if N is not None else w.N)
-                               if w.tree == "chain" else w.max_depth)
+    n = N if N is not None else w.N
+    return dataclasses.replace(w, B=B if B is not None else w.B, H=H if H is not None else w.H,
+                               N=n, max_depth=n if w.tree == "chain" else w.max_depth)
 
 
 # --------------------------------------------------------------------------

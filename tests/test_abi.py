@@ -1,0 +1,95 @@
+"""The C-ABI library loads, exports what include/treewy.h declares, and its
+host-side checks return the documented status codes (no kernel runs here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "treewy.h")
+
+
+@pytest.fixture(scope="module")
+def tw():
+    from paper_2608_20961_amd import treewy
+    return treewy
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(treewy_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    assert names == sorted(["treewy_verify", "treewy_commit", "treewy_snapshot_verify",
+                            "treewy_snapshot_commit", "treewy_path_from_node", "treewy_status_string"])
+
+
+def test_library_exports_every_declared_symbol(tw):
+    for name in declared_functions():
+        assert hasattr(tw.lib, name), name
+    assert set(tw.EXPORTED) == set(declared_functions())
+
+
+def test_status_strings(tw):
+    for s in range(4):
+        assert tw.lib.treewy_status_string(s)
+    assert tw.lib.treewy_status_string(99) == b"unknown status"
+
+
+A = ctypes.c_void_p(16)   # aligned stand-in pointers: never dereferenced by the host checks
+M = ctypes.c_void_p(18)   # misaligned
+
+
+def _verify(tw, fn="treewy_verify", S0=A, q=A, N=8, B=2, H=2, dk=128, dv=128, dt=1, o=A, U=A):
+    return getattr(tw.lib, fn)(S0, q, A, A, A, A, A, N, B, H, dk, dv, dt, o, U, None, None)
+
+
+@pytest.mark.parametrize("fn", ["treewy_verify", "treewy_snapshot_verify"])
+def test_verify_host_checks(tw, fn):
+    assert _verify(tw, fn, dk=64) == tw.TREEWY_ERR_UNSUPPORTED
+    assert _verify(tw, fn, dv=96) == tw.TREEWY_ERR_UNSUPPORTED
+    assert _verify(tw, fn, N=65) == tw.TREEWY_ERR_UNSUPPORTED
+    assert _verify(tw, fn, N=-1) == tw.TREEWY_ERR_INVALID_ARG
+    assert _verify(tw, fn, B=-3) == tw.TREEWY_ERR_INVALID_ARG
+    assert _verify(tw, fn, dt=7) == tw.TREEWY_ERR_INVALID_ARG
+    assert _verify(tw, fn, S0=None) == tw.TREEWY_ERR_INVALID_ARG
+    assert _verify(tw, fn, U=None) == tw.TREEWY_ERR_INVALID_ARG
+    assert _verify(tw, fn, S0=M) == tw.TREEWY_ERR_INVALID_ARG
+    # nothing to do: returns before touching any pointer or the GPU
+    assert _verify(tw, fn, N=0, S0=None) == tw.TREEWY_OK
+    assert _verify(tw, fn, B=0, S0=None) == tw.TREEWY_OK
+    assert _verify(tw, fn, H=0, S0=None) == tw.TREEWY_OK
+
+
+def test_commit_host_checks(tw):
+    f = tw.lib.treewy_commit
+
+    def call(S0=A, path=A, plen=A, L_max=8, N=8, B=2, H=2, dk=128, dt=1, S_new=A):
+        return f(S0, A, A, A, path, plen, L_max, None, N, B, H, dk, 128, dt, S_new, None, None)
+
+    assert call(dk=64) == tw.TREEWY_ERR_UNSUPPORTED
+    assert call(L_max=65) == tw.TREEWY_ERR_UNSUPPORTED
+    assert call(L_max=-1) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(plen=None) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(path=None) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(S_new=M) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(dt=2) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(B=0, S0=None) == tw.TREEWY_OK
+
+
+def test_snapshot_commit_and_path_host_checks(tw):
+    assert tw.lib.treewy_snapshot_commit(A, A, None, 8, 2, 2, 128, 128, A, None, None) == tw.TREEWY_ERR_INVALID_ARG
+    assert tw.lib.treewy_snapshot_commit(A, A, A, 8, 2, 2, 128, 64, A, None, None) == tw.TREEWY_ERR_UNSUPPORTED
+    assert tw.lib.treewy_path_from_node(A, A, 65, 2, 8, A, A, None, None) == tw.TREEWY_ERR_UNSUPPORTED
+    assert tw.lib.treewy_path_from_node(A, None, 8, 2, 8, A, A, None, None) == tw.TREEWY_ERR_INVALID_ARG
+    assert tw.lib.treewy_path_from_node(None, None, 8, 0, 8, None, None, None, None) == tw.TREEWY_OK
+
+
+def test_binding_raises_with_status(tw):
+    with pytest.raises(tw.TreewyError) as e:
+        tw._check(tw.TREEWY_ERR_UNSUPPORTED, "treewy_verify")
+    assert e.value.status == tw.TREEWY_ERR_UNSUPPORTED and "unsupported" in str(e.value)
