@@ -1,0 +1,289 @@
+"""Benchmark: tree-WY verify + commit of one GDN layer on one MI355X.
+
+A step is one pass of the hot path over one batch: treewy_verify (every draft
+node's output and the pseudo-values, one solve per (sequence, head)) followed
+by treewy_commit (the accepted node's state, out of place so the inputs stay
+fixed).  The default workload is the 397B-shaped wide tree: B = 128 sequences,
+H = 64 value heads, d_k = d_v = 128, N = 64 draft nodes (max depth 8), bf16
+q/k/v and fp32 state.  Inputs are resident in HBM before the timed region.
+
+Prints ONE JSON line.  Besides the headline (verified draft nodes per second
+for the layer) it carries the per-kernel HBM rooflines, the full-state-
+snapshot baseline on the same workload, and the float64 oracle timed on the
+host's cores as a CPU baseline.
+
+  python bench.py [--steps K] [--warmup W] [--workload 0..4] [--gpus 1]
+                  [--no-snapshot] [--no-cpu-baseline] [--copy-calibration]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E, vendor figure
+METRIC = "verified draft nodes/sec per GDN layer + commit GB/s (% HBM peak), 1 GPU"
+
+
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--workload", type=int, default=3)
+    p.add_argument("--seed", type=int, default=0)
+    p.add_argument("--no-snapshot", action="store_true")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time for the CPU baseline")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="only run a plain 1 GiB device copy (for scaling HBM counters)")
+    return p.parse_args()
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_20961_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel: str, workload: str, src_hash: str):
+    """HBM bytes per launch from committed rocprofv3 counter summaries, if they
+    were taken on the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", "traffic_%s_%s.txt" % (kernel, workload))
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            key, val = line.split(":", 1)
+            vals[key.strip()] = val.strip()
+    if vals.get("source_hash") != src_hash:
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration(torch):
+    n = 1 << 28                                    # 2^28 floats = 1 GiB
+    src = torch.ones(n, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_each_way": 4 * n, "launches": 5}), flush=True)
+
+
+def device_inputs(torch, tw, wl, w, seed):
+    """Seeded inputs on the device; S0 made on the device by running verify +
+    commit over warm-up chains of 32 float32 tokens (the committed state of
+    each chunk is the next chunk's S0).  The warm-up uses the float32, N <= 32
+    kernels, so a profile's per-kernel statistics for the timed bf16 kernels
+    cover only the timed launches."""
+    dev = torch.device("cuda:0")
+    dt = torch.bfloat16 if w.in_dtype == "bf16" else torch.float32
+    x = wl.make_inputs(w, seed=seed)
+
+    def put(a, dtype):
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dtype)
+
+    d = dict(q=put(x["q"], dt), k=put(x["k"], dt), v=put(x["v"], dt), alpha=put(x["alpha"], torch.float32),
+             beta=put(x["beta"], torch.float32), parent=put(x["parent"], torch.int32),
+             path=put(x["path"], torch.int32), path_len=put(x["path_len"], torch.int32))
+    S = torch.zeros((w.B, w.H, w.d_v, w.d_k), dtype=torch.float32, device=dev)
+    T = 32
+    chunks = (w.warm_tokens + T - 1) // T
+    for c in range(chunks):
+        Tc = min(T, w.warm_tokens - c * T)
+        k, v, a, b = wl.warmup_chunk_torch(w, seed, c, Tc, dev, torch.float32)
+        par = torch.arange(-1, Tc - 1, dtype=torch.int32, device=dev).repeat(w.B, 1).contiguous()
+        path = torch.arange(Tc, dtype=torch.int32, device=dev).repeat(w.B, 1).contiguous()
+        plen = torch.full((w.B,), Tc, dtype=torch.int32, device=dev)
+        _, U = tw.treewy_verify(S, k, k, v, a, b, par)
+        S = tw.treewy_commit(S, U, k, a, path, plen, parent=par, S_new=S)
+    torch.cuda.synchronize()
+    d["S0"] = S
+    return x, d
+
+
+def time_steps(torch, launches, steps, warmup):
+    """Run `launches` (a list of callables, one step) W + K times; return the
+    average step time and the average time of each launch (HIP events on the
+    stream the kernels run on)."""
+    for _ in range(warmup):
+        for f in launches:
+            f()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(launches) + 1)] for _ in range(steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for i in range(steps):
+        ev[i][0].record(stream)
+        for j, f in enumerate(launches):
+            f()
+            ev[i][j + 1].record(stream)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    total = t0.elapsed_time(t1) / steps
+    per = [float(np.mean([ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(steps)])) for j in range(len(launches))]
+    return total, per
+
+
+def roofline(bytes_per_launch, ms, traffic):
+    gbps = bytes_per_launch / (ms * 1e-3) / 1e9
+    return {"bound": "hbm", "achieved": round(gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+            "frac": round(gbps / PEAK_HBM_GBPS, 4), "traffic": traffic,
+            "algorithmic_bytes": int(bytes_per_launch), "avg_launch_ms": round(ms, 5)}
+
+
+def cpu_baseline(w, wl, x, seed, target_s):
+    """The float64 oracle (verify + commit) on a bounded sample of units.
+
+    S0 of each sampled unit is the oracle's own warm-up over the unit's
+    warm-up tokens (untimed); the timed part is verify + commit."""
+    import oracle
+    orc = oracle.default()
+    H, N = w.H, w.N
+
+    def warm(units):
+        S0 = np.empty((len(units), w.d_v, w.d_k))
+        for lo in range(0, len(units), 256):
+            part = units[lo:lo + 256]
+            toks = [wl.warmup_tokens(w, seed=seed, units=slice(int(u), int(u) + 1)) for u in part]
+            cat = {n: np.concatenate([t[n] for t in toks]) for n in ("k", "v", "alpha", "beta")}
+            S0[lo:lo + len(part)] = orc.chain(np.zeros((len(part), w.d_v, w.d_k)), cat["k"], cat["v"],
+                                              cat["alpha"], cat["beta"])
+        return S0.astype(np.float32)
+
+    def run(units, S0):
+        b = units // H
+        sel = lambda a: a.reshape(w.units, *a.shape[2:])[units].astype(np.float64)
+        q, k, v, al, be = (sel(x[n]) for n in ("q", "k", "v", "alpha", "beta"))
+        par = x["parent"][b]
+        t0 = time.perf_counter()
+        orc.verify(S0, q, k, v, al, be, par)
+        orc.commit(S0, k, v, al, be, par, x["path"][b], x["path_len"][b])
+        return time.perf_counter() - t0
+
+    probe = np.arange(min(64, w.units))
+    dt = run(probe, warm(probe))
+    count = int(min(w.units, max(len(probe), len(probe) * target_s / max(dt, 1e-6))))
+    units = wl.sample_units(w, count, seed=1)
+    dt = run(units, warm(units))
+    nodes_per_s = (len(units) / H) * N / dt       # a sequence's N nodes cost H units of work
+    return {"value": round(nodes_per_s, 1), "unit": "nodes/s", "cores": orc.threads(), "kind": "oracle",
+            "sample": "%d of %d (sequence, head) units of the same workload; float64 verify + commit "
+                      "took %.2f s; nodes/s = units/H * N / time" % (len(units), w.units, dt)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs on exactly one GPU: the verify/commit path has no cross-GPU step "
+              "and this build measures one GPU's share (got --gpus %d)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if args.copy_calibration:
+        copy_calibration(torch)
+        return
+    from paper_2608_20961_amd import accounting as acc
+    from paper_2608_20961_amd import treewy as tw
+    from paper_2608_20961_amd import workload as wl
+
+    w = wl.WORKLOADS[args.workload]
+    log("workload " + w.describe())
+    x, d = device_inputs(torch, tw, wl, w, args.seed)
+    log("inputs resident, S0 warmed on the device")
+    U = torch.empty((w.B, w.H, w.N, w.d_v), dtype=torch.float32, device="cuda")
+    o = torch.empty((w.B, w.H, w.N, w.d_v), dtype=d["q"].dtype, device="cuda")
+    S_new = torch.empty_like(d["S0"])
+
+    def verify():
+        tw.treewy_verify(d["S0"], d["q"], d["k"], d["v"], d["alpha"], d["beta"], d["parent"], o=o, U=U)
+
+    def commit():
+        tw.treewy_commit(d["S0"], U, d["k"], d["alpha"], d["path"], d["path_len"], parent=d["parent"], S_new=S_new)
+
+    ms_step, (ms_verify, ms_commit) = time_steps(torch, [verify, commit], args.steps, args.warmup)
+    log("timed %d steps: %.4f ms/step (verify %.4f, commit %.4f)" % (args.steps, ms_step, ms_verify, ms_commit))
+    src_hash = kernel_source_hash()
+    vb = acc.verify_bytes(w)
+    cb = acc.commit_bytes(w, x["path_len"])
+    rf_verify = roofline(vb, ms_verify, load_traffic("verify", w.name, src_hash))
+    rf_commit = roofline(cb, ms_commit, load_traffic("commit", w.name, src_hash))
+    dominant = rf_verify if ms_verify >= ms_commit else rf_commit
+    nodes = w.B * w.N
+    result = {
+        "metric": METRIC,
+        "value": round(nodes / (ms_step * 1e-3), 1),
+        "unit": "nodes/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": w.in_dtype, "data": "synthetic",
+        "config": {"workload": w.describe(), "B": w.B, "H": w.H, "N": w.N, "d_k": w.d_k, "d_v": w.d_v,
+                   "step": "treewy_verify + treewy_commit (out of place)", "accumulate": "f32",
+                   "state": "f32", "parallelism": "none (1 GPU)"},
+        "roofline": dict(dominant, kernel="treewy_verify" if dominant is rf_verify else "treewy_commit"),
+        "verify": dict(rf_verify, nodes_per_s=round(nodes / (ms_verify * 1e-3), 1),
+                       head_nodes_per_s=round(w.units * w.N / (ms_verify * 1e-3), 1),
+                       useful_tflops=round(acc.verify_flops(w) / (ms_verify * 1e-3) / 1e12, 2)),
+        "commit": dict(rf_commit, pct_hbm_peak=round(100 * rf_commit["frac"], 2)),
+        "kernel_source_hash": src_hash,
+    }
+    spec = acc.speculative_state_bytes(w)
+    result["speculative_state_bytes"] = {"treewy_U": spec["treewy_U"], "treewy_U_k_alpha": spec["treewy_U_k_alpha"],
+                                         "snapshot_states": spec["snapshot_states"]}
+    if not args.no_snapshot:
+        snaps = torch.empty((w.B, w.H, w.N, w.d_v, w.d_k), dtype=torch.float32, device="cuda")
+        acc_node = torch.tensor([int(x["path"][b, x["path_len"][b] - 1]) if x["path_len"][b] else -1
+                                 for b in range(w.B)], dtype=torch.int32, device="cuda")
+        o2 = torch.empty_like(o)
+
+        def sverify():
+            tw.treewy_snapshot_verify(d["S0"], d["q"], d["k"], d["v"], d["alpha"], d["beta"], d["parent"],
+                                      o=o2, snapshots=snaps)
+
+        def scommit():
+            tw.treewy_snapshot_commit(d["S0"], snaps, acc_node, S_new=S_new)
+
+        ss = max(3, args.steps // 10)
+        ms_s, (ms_sv, ms_sc) = time_steps(torch, [sverify, scommit], ss, 1)
+        sb = acc.snapshot_verify_bytes(w)
+        result["snapshot_baseline"] = {
+            "ms_per_step": round(ms_s, 4), "steps": ss,
+            "nodes_per_s": round(nodes / (ms_s * 1e-3), 1),
+            "verify": roofline(sb, ms_sv, None), "commit": roofline(acc.snapshot_commit_bytes(w), ms_sc, None),
+            "speculative_state_bytes": spec["snapshot_states"],
+            "treewy_speedup": round(ms_s / ms_step, 2),
+        }
+        del snaps
+        log("snapshot baseline: %.4f ms/step" % ms_s)
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        result["cpu_baseline"] = cpu_baseline(w, wl, x, args.seed, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

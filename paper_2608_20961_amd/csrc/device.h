@@ -13,6 +13,7 @@ constexpr int THREADS = 256;    // four wave64s per workgroup
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -42,6 +43,46 @@ __device__ __forceinline__ bf16x8 round8(const float *x) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) h[e] = (__bf16)x[e];
     return h;
+}
+
+// Raw buffer view of `bytes` bytes at `base` (the descriptor lives in SGPRs).
+// Loads at offsets past the end return zero and stores there are dropped, so
+// the ragged tail of a tile needs no branch.  The range check covers the
+// per-lane offset plus the instruction offset.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+__device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ f32x4 ld_f32x4(rsrc_t r, int off) {
+    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ uint4 ld_u32x4(rsrc_t r, int off) {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ float ld_f32(rsrc_t r, int off) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+__device__ __forceinline__ int ld_i32(rsrc_t r, int off) {
+    return __builtin_bit_cast(int, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+__device__ __forceinline__ __bf16 ld_bf16(rsrc_t r, int off) {
+    return __builtin_bit_cast(__bf16, __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0));
+}
+template <typename T> __device__ __forceinline__ T ld_elem(rsrc_t r, int off);
+template <> __device__ __forceinline__ float ld_elem<float>(rsrc_t r, int off) { return ld_f32(r, off); }
+template <> __device__ __forceinline__ __bf16 ld_elem<__bf16>(rsrc_t r, int off) { return ld_bf16(r, off); }
+__device__ __forceinline__ void st_u32x4(rsrc_t r, int off, uint4 x) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned int, x),
+                                           r, off, 0, 0);
+}
+__device__ __forceinline__ void st_f32(rsrc_t r, int off, float x) {
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned int, x), r, off, 0, 0);
+}
+
+// A copy of x the compiler cannot see through (keeps derived values inside a loop).
+__device__ __forceinline__ int opaque(int x) {
+    asm volatile("" : "+v"(x));
+    return x;
 }
 
 __device__ __forceinline__ float to_f32(float x) { return x; }

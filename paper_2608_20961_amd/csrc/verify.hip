@@ -1,4 +1,6 @@
-// treewy_verify kernel: one workgroup (four wave64s) per (sequence, head).
+// treewy_verify kernel: one workgroup (four wave64s) per (sequence, head) unit
+// at a time; the grid is sized to the resident capacity of the GPU and every
+// workgroup walks a strided list of units.
 //
 // The method (Method, eq. 2 and the read-out of the same solve), per unit:
 //   g_t    = product of alpha over t and its ancestors
@@ -17,7 +19,13 @@
 // lane of wave 0 builds one row of T independently (work ~ depth^2).  U = T R
 // and A U then run on the matrix cores with R and U taken straight from the
 // accumulator registers (the contraction index is permuted to match the
-// accumulator layout; T and A are read in the same permuted order).
+// accumulator layout; T and A are read in the same permuted order).  U and O
+// leave through LDS as whole-row 16-byte stores.
+//
+// Streaming.  All of a unit's HBM reads are issued at once, in the order they
+// are consumed (tree and gates, K/Q, V, then S0), through buffer descriptors
+// bounded to the unit so padding rows read as zero without branches; two
+// workgroups per CU keep HBM busy while the other one computes.
 //
 // Precision.  The matrix cores take bf16; fp32 operands are split into
 // hi + lo bf16 pairs and multiplied in three passes (hi*hi + hi*lo + lo*hi),
@@ -32,42 +40,103 @@ template <int NP, bool F32IN>
 struct VerifyLds {
     static constexpr int XS = D + 8;                    // bf16 per staged K/Q row (pad breaks bank aliasing)
     static constexpr int MS = NP + 4;                   // floats per row of the N x N matrices
+    static constexpr int US = D + 4;                    // floats per staged U row
+    static constexpr int OS = D + 8;                    // bf16 per staged o row
     static constexpr int X_BYTES = 2 * NP * XS * 2;     // [K; Q] in bf16
     static constexpr int XLO_OFF = X_BYTES;             // low halves of fp32 K/Q
     static constexpr int B_OFF = X_BYTES * (F32IN ? 2 : 1);
     static constexpr int M_BYTES = NP * MS * 4;
     static constexpr int A_OFF = B_OFF + M_BYTES;
-    static constexpr int ALPHA_OFF = A_OFF + M_BYTES;
-    static constexpr int BETA_OFF = ALPHA_OFF + NP * 4;
+    static constexpr int BETA_OFF = A_OFF + M_BYTES;
     static constexpr int G_OFF = BETA_OFF + NP * 4;
-    static constexpr int PAR_OFF = G_OFF + NP * 4;
-    static constexpr int ANC_OFF = PAR_OFF + NP * 4;
-    static constexpr int BYTES = ANC_OFF + NP * 8;
+    static constexpr int ANC_OFF = G_OFF + NP * 4;
+    static constexpr int END = ANC_OFF + NP * 8;
+    static constexpr bool O_IN_B = NP * OS * 2 <= M_BYTES;   // o staged where B was, else appended
+    static constexpr int O_OFF = O_IN_B ? B_OFF : END;
+    static constexpr int END_O = (O_IN_B || F32IN) ? END : END + NP * OS * 2;
+    static constexpr int V_BYTES = NP * D * (F32IN ? 4 : 2);
+    static constexpr bool V_IN_BA = V_BYTES <= 2 * M_BYTES;  // V staged over B and A before the gram
+    static constexpr int V_OFF = V_IN_BA ? B_OFF : END_O;
+    static constexpr int BYTES = V_IN_BA ? END_O : END_O + V_BYTES;
     static_assert(NP * MS * 4 <= X_BYTES, "T must fit where K/Q were staged");
-    static_assert(B_OFF % 16 == 0 && A_OFF % 16 == 0 && ANC_OFF % 8 == 0, "alignment");
+    static_assert(NP * US * 4 <= B_OFF, "U staging must fit where K/Q were staged");
+    static_assert(B_OFF % 16 == 0 && A_OFF % 16 == 0 && ANC_OFF % 8 == 0 && O_OFF % 16 == 0 &&
+                  V_OFF % 16 == 0, "alignment");
+};
+
+// One unit's HBM reads, held in registers from issue to use.  Every read goes
+// through a buffer descriptor bounded to this unit's rows, so rows of padding
+// nodes (t >= N) read as zero.
+template <int NP, bool F32IN>
+struct UnitReads {
+    using In = typename std::conditional<F32IN, float, __bf16>::type;
+    static constexpr int MT = NP / 32;
+    static constexpr int CHUNK = F32IN ? 4 : 8;         // elements per 16-byte chunk
+    static constexpr int CPR = D / CHUNK;               // chunks per row
+    static constexpr int KQN = 2 * NP * CPR / THREADS;  // K/Q chunks per thread
+    static constexpr int KN = KQN / 2;                  // the first KN are K, the rest Q
+    static constexpr int ROW = D * (int)sizeof(In);     // bytes per q/k/v row
+    int par;                                            // wave 0, node = lane
+    float al, be;
+    uint4 kq[KQN];                                      // chunk i: row (tid / CPR + i THREADS / CPR) mod NP
+    f32x4 s0[8][2];                                     // S0 row `col`, d_k [16s + 8hg, +8)
+    static constexpr int VQN = NP * ROW / 16 / THREADS;  // V chunks per thread
+    uint4 vq[VQN];                                      // V rows, 16 bytes per chunk, coalesced
+
+    // Every HBM read of unit u, in the order the unit consumes them.
+    __device__ __forceinline__ void issue(const float *S0, const In *q, const In *k, const In *vv,
+                                          const float *alpha, const float *beta, const int32_t *parent,
+                                          int u, int b, int N, int tid, int lane, int wave, int hg,
+                                          int col) {
+        const size_t node0 = (size_t)u * N;
+        if (wave == 0) {
+            par = ld_i32(make_rsrc(parent + (size_t)b * N, N * 4), lane * 4);
+            al = ld_f32(make_rsrc(alpha + node0, N * 4), lane * 4);
+            be = ld_f32(make_rsrc(beta + node0, N * 4), lane * 4);
+        }
+        const rsrc_t rk = make_rsrc(k + node0 * D, N * ROW), rq = make_rsrc(q + node0 * D, N * ROW);
+#pragma unroll
+        for (int i = 0; i < KQN; ++i) {
+            const int idx = tid + THREADS * i, r = idx / CPR, c = (idx % CPR) * CHUNK;
+            const int t = i < KN ? r : r - NP;
+            kq[i] = ld_u32x4(i < KN ? rk : rq, t * ROW + c * (int)sizeof(In));
+        }
+        const rsrc_t rv = make_rsrc(vv + node0 * D, N * ROW);
+#pragma unroll
+        for (int i = 0; i < VQN; ++i) vq[i] = ld_u32x4(rv, (tid + THREADS * i) * 16);
+        const rsrc_t rs = make_rsrc(S0 + (size_t)u * D * D, D * D * 4);
+        const int base = (col * D + 8 * hg) * 4;
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+            s0[s][0] = ld_f32x4(rs, base + 64 * s);
+            s0[s][1] = ld_f32x4(rs, base + 64 * s + 16);
+        }
+    }
 };
 
 template <int NP, bool F32IN>
-__global__ __launch_bounds__(THREADS, 2) void verify_kernel(
+__global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_kernel(
     const float *__restrict__ S0, const void *__restrict__ q_, const void *__restrict__ k_,
     const void *__restrict__ v_, const float *__restrict__ alpha, const float *__restrict__ beta,
-    const int32_t *__restrict__ parent, int N, int H, void *__restrict__ o_, float *__restrict__ U,
-    int32_t *__restrict__ err) {
+    const int32_t *__restrict__ parent, int N, int H, int units, void *__restrict__ o_,
+    float *__restrict__ U, int32_t *__restrict__ err) {
     using In = typename std::conditional<F32IN, float, __bf16>::type;
     using L = VerifyLds<NP, F32IN>;
+    using Reads = UnitReads<NP, F32IN>;
     constexpr int MT = NP / 32;                          // 32-row tiles of nodes
-    constexpr int XS = L::XS, MS = L::MS;
+    constexpr int XS = L::XS, MS = L::MS, US = L::US, OS = L::OS;
+    constexpr int CHUNK = Reads::CHUNK, CPR = Reads::CPR, KQN = Reads::KQN;
 
     __shared__ __attribute__((aligned(16))) unsigned char lds[L::BYTES];
     __bf16 *Xh = reinterpret_cast<__bf16 *>(lds);
     __bf16 *Xl = reinterpret_cast<__bf16 *>(lds + L::XLO_OFF);
     float *Bm = reinterpret_cast<float *>(lds + L::B_OFF);
     float *Am = reinterpret_cast<float *>(lds + L::A_OFF);
-    float *Tm = reinterpret_cast<float *>(lds);          // reuses the K/Q area once P is done
-    float *al_s = reinterpret_cast<float *>(lds + L::ALPHA_OFF);
+    float *Tm = reinterpret_cast<float *>(lds);          // T reuses the K/Q area once P is done,
+    float *Us = reinterpret_cast<float *>(lds);          // then U is staged there
+    __bf16 *Os = reinterpret_cast<__bf16 *>(lds + L::O_OFF);   // o staging (bf16 input only)
     float *be_s = reinterpret_cast<float *>(lds + L::BETA_OFF);
     float *g_s = reinterpret_cast<float *>(lds + L::G_OFF);
-    int *par_s = reinterpret_cast<int *>(lds + L::PAR_OFF);
     uint64_t *anc_s = reinterpret_cast<uint64_t *>(lds + L::ANC_OFF);
 
     const In *q = static_cast<const In *>(q_);
@@ -75,284 +144,388 @@ __global__ __launch_bounds__(THREADS, 2) void verify_kernel(
     const In *v = static_cast<const In *>(v_);
     In *o = static_cast<In *>(o_);
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int l32 = lane & 31, hg = lane >> 5;
-    const int u = blockIdx.x, b = u / H;
-    const size_t node0 = (size_t)u * N;                  // row of node 0 of this unit in q/k/v/o/U
-    const int col = wave * 32 + l32;                     // this lane's d_v column (= row of S0)
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 
-    // ---- phase 0: issue every HBM read of the unit -------------------------
-    // S0 rows of this wave as matrix-core B operands: step s covers d_k [16s, 16s+16).
-    f32x4 s0r[8][2];
-    {
-        const float *src = S0 + (size_t)u * D * D + (size_t)col * D + 8 * hg;
-#pragma unroll
-        for (int s = 0; s < 8; ++s) {
-            s0r[s][0] = *reinterpret_cast<const f32x4 *>(src + 16 * s);
-            s0r[s][1] = *reinterpret_cast<const f32x4 *>(src + 16 * s + 4);
-        }
-    }
-    // V at the accumulator positions of P_K.
-    float vr[MT][16];
-#pragma unroll
-    for (int m = 0; m < MT; ++m)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int t = 32 * m + acc_row(r, hg);
-            vr[m][r] = t < N ? to_f32(v[(node0 + t) * D + col]) : 0.f;
-        }
-    if (tid < NP) {
-        const int t = tid;
-        al_s[t] = t < N ? alpha[node0 + t] : 1.f;
-        be_s[t] = t < N ? beta[node0 + t] : 0.f;
-        par_s[t] = t < N ? parent[(size_t)b * N + t] : -1;
-        g_s[t] = 0.f;
-        anc_s[t] = 0;
-    }
-    // K rows [0, NP) and Q rows [NP, 2NP) into LDS as bf16 (hi/lo for fp32 input).
-    if constexpr (!F32IN) {
-        for (int idx = tid; idx < 2 * NP * 16; idx += THREADS) {
-            const int r = idx >> 4, c = (idx & 15) * 8;
-            const int t = r < NP ? r : r - NP;
-            const In *src = r < NP ? k : q;
-            uint4 val = {0u, 0u, 0u, 0u};
-            if (t < N) val = *reinterpret_cast<const uint4 *>(src + (node0 + t) * D + c);
-            *reinterpret_cast<uint4 *>(Xh + r * XS + c) = val;
-        }
-    } else {
-        for (int idx = tid; idx < 2 * NP * 32; idx += THREADS) {
-            const int r = idx >> 5, c = (idx & 31) * 4;
-            const int t = r < NP ? r : r - NP;
-            const In *src = r < NP ? k : q;
-            f32x4 val = {0.f, 0.f, 0.f, 0.f};
-            if (t < N) val = *reinterpret_cast<const f32x4 *>(src + (node0 + t) * D + c);
-            bf16x4 hi, lo;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                hi[e] = (__bf16)val[e];
-                lo[e] = (__bf16)(val[e] - (float)hi[e]);
+    Reads rd;
+    int u = blockIdx.x;
+    for (; u < units; u += gridDim.x) {
+        // Lane indices are re-derived each iteration from an opaque copy so the
+        // per-lane offsets below are recomputed here instead of being hoisted
+        // out of the loop and held in registers for its whole length.
+        const int tid = opaque(threadIdx.x), lane = tid & 63;
+        const int l32 = lane & 31, hg = lane >> 5;
+        const int col = wave * 32 + l32;                 // this lane's d_v column (= row of S0)
+        const int b = u / H;
+        const size_t node0 = (size_t)u * N;              // row of node 0 of this unit in q/k/v/o/U
+        rd.issue(S0, q, k, v, alpha, beta, parent, u, b, N, tid, lane, wave, hg, col);
+
+        // ---- phase 1: ancestors and cumulative decay by pointer jumping ----
+        // Lane t of wave 0 keeps (ptr, prod, mask): ptr an ancestor of t (or
+        // -1), prod the product of alpha over the path (ptr, t], mask the
+        // ancestors of t strictly below t down to and including ptr.  Each
+        // round doubles the covered path by reading the state of lane ptr, so
+        // depth d needs ceil(log2 d) rounds; then prod = g_t, mask = ancestors.
+        if (wave == 0) {
+            int ptr = lane < N ? rd.par : -1;
+            if (lane < N && (ptr < -1 || ptr >= lane)) {
+                flag_error(err, b, TREEWY_FLAG_BAD_PARENT);
+                ptr = -1;
             }
-            *reinterpret_cast<bf16x4 *>(Xh + r * XS + c) = hi;
-            *reinterpret_cast<bf16x4 *>(Xl + r * XS + c) = lo;
-        }
-    }
-    {
-        uint4 *z = reinterpret_cast<uint4 *>(lds + L::B_OFF);
-        for (int idx = tid; idx < 2 * L::M_BYTES / 16; idx += THREADS) z[idx] = uint4{0u, 0u, 0u, 0u};
-    }
-    __syncthreads();
-
-    // ---- phase 1: walk each node's ancestors (wave 0, lane t) -------------
-    // Row t of Bm temporarily holds the decay ratios g_t/g_i of t's ancestors
-    // (1 on the diagonal); g_t and the ancestor bit mask go to g_s / anc_s.
-    if (wave == 0 && lane < N) {
-        const int t = lane;
-        Bm[t * MS + t] = 1.f;
-        float ratio = 1.f;
-        uint64_t mask = 0;
-        bool bad = false;
-        for (int cur = t;;) {
-            ratio *= al_s[cur];
-            int p = par_s[cur];
-            if (p < -1 || p >= cur) {
-                bad = true;
-                p = -1;
+            float prod = lane < N ? rd.al : 0.f;
+            uint64_t mask = ptr >= 0 ? (1ull << ptr) : 0ull;
+            while (__any(ptr >= 0)) {
+                const int src = ptr >= 0 ? ptr : lane;
+                const float prod_s = __shfl(prod, src);
+                const int ptr_s = __shfl(ptr, src);
+                const uint64_t mask_s = __shfl(mask, src);
+                if (ptr >= 0) {
+                    prod *= prod_s;
+                    mask |= mask_s;
+                    ptr = ptr_s;
+                }
             }
-            if (p < 0) break;
-            Bm[t * MS + p] = ratio;
-            mask |= 1ull << p;
-            cur = p;
-        }
-        g_s[t] = ratio;
-        anc_s[t] = mask;
-        if (bad) flag_error(err, b, TREEWY_FLAG_BAD_PARENT);
-    }
-    __syncthreads();
-
-    // ---- phase 2: masked, decay-weighted gram tiles (lower triangle) ------
-    constexpr int NPAIRS = MT * (MT + 1) / 2;
-    if (wave < NPAIRS) {
-        const int mt = wave == 0 ? 0 : 1;
-        const int nt = wave == 2 ? 1 : 0;
-        f32x16 gkk = {}, gqk = {};
-        const __bf16 *ak_row = Xh + (32 * mt + l32) * XS + 8 * hg;
-        const __bf16 *aq_row = Xh + (NP + 32 * mt + l32) * XS + 8 * hg;
-        const __bf16 *bk_row = Xh + (32 * nt + l32) * XS + 8 * hg;
-#pragma unroll
-        for (int s = 0; s < 8; ++s) {
-            const bf16x8 ak = *reinterpret_cast<const bf16x8 *>(ak_row + 16 * s);
-            const bf16x8 aq = *reinterpret_cast<const bf16x8 *>(aq_row + 16 * s);
-            const bf16x8 bk = *reinterpret_cast<const bf16x8 *>(bk_row + 16 * s);
-            gkk = mma(ak, bk, gkk);
-            gqk = mma(aq, bk, gqk);
-            if constexpr (F32IN) {
-                const ptrdiff_t lo = Xl - Xh;
-                const bf16x8 akl = *reinterpret_cast<const bf16x8 *>(ak_row + lo + 16 * s);
-                const bf16x8 aql = *reinterpret_cast<const bf16x8 *>(aq_row + lo + 16 * s);
-                const bf16x8 bkl = *reinterpret_cast<const bf16x8 *>(bk_row + lo + 16 * s);
-                gkk = mma(ak, bkl, gkk);
-                gkk = mma(akl, bk, gkk);
-                gqk = mma(aq, bkl, gqk);
-                gqk = mma(aql, bk, gqk);
+            if (lane < NP) {
+                g_s[lane] = prod;
+                be_s[lane] = lane < N ? rd.be : 0.f;
+                anc_s[lane] = mask;
             }
         }
-        const int i = 32 * nt + l32;
+        // K and Q into LDS as bf16 (hi/lo for fp32 input), padding rows zero.
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int t = 32 * mt + acc_row(r, hg);
-            const float dr = Bm[t * MS + i];
-            Bm[t * MS + i] = i < t ? be_s[t] * dr * gkk[r] : 0.f;
-            Am[t * MS + i] = dr * gqk[r];
-        }
-    }
-
-    // ---- phase 3: P = [K; Q] S0^T for this wave's 32 columns --------------
-    f32x16 accp[2 * MT];
+        for (int i = 0; i < KQN; ++i) {
+            const int idx = tid + THREADS * i, r = idx / CPR, c = (idx % CPR) * CHUNK;
+            const uint4 val = rd.kq[i];
+            if constexpr (!F32IN) {
+                *reinterpret_cast<uint4 *>(Xh + r * XS + c) = val;
+            } else {
+                const f32x4 f = *reinterpret_cast<const f32x4 *>(&val);
+                bf16x4 hi, lo;
 #pragma unroll
-    for (int m = 0; m < 2 * MT; ++m) accp[m] = f32x16{};
-#pragma unroll
-    for (int s = 0; s < 8; ++s) {
-        float sv[8];
-        *reinterpret_cast<f32x4 *>(sv) = s0r[s][0];
-        *reinterpret_cast<f32x4 *>(sv + 4) = s0r[s][1];
-        bf16x8 bh, bl;
-        split8(sv, bh, bl);
-#pragma unroll
-        for (int m = 0; m < 2 * MT; ++m) {
-            const __bf16 *arow = Xh + (32 * m + l32) * XS + 16 * s + 8 * hg;
-            const bf16x8 a = *reinterpret_cast<const bf16x8 *>(arow);
-            accp[m] = mma(a, bh, accp[m]);
-            accp[m] = mma(a, bl, accp[m]);
-            if constexpr (F32IN) {
-                const bf16x8 alo = *reinterpret_cast<const bf16x8 *>(arow + (Xl - Xh));
-                accp[m] = mma(alo, bh, accp[m]);
+                for (int e = 0; e < 4; ++e) {
+                    hi[e] = (__bf16)f[e];
+                    lo[e] = (__bf16)(f[e] - (float)hi[e]);
+                }
+                *reinterpret_cast<bf16x4 *>(Xh + r * XS + c) = hi;
+                *reinterpret_cast<bf16x4 *>(Xl + r * XS + c) = lo;
             }
         }
-    }
-    __syncthreads();
-
-    // ---- phase 4: rows of T = (I + B)^{-1} (wave 0); R and g P_Q (all) ----
-    // (T (I + B))[t, j] = 0 for j != t gives, walking t's ancestors j from
-    // the nearest upwards, T[t, j] = -sum over i in {t} and the ancestors of
-    // t below j of T[t, i] B[i, j], with T[t, t] = 1.
-    if (wave == 0) {
-        if (lane < NP) {
-            f32x4 *row = reinterpret_cast<f32x4 *>(Tm + lane * MS);
+        // V rows into LDS as loaded (rows of padding nodes are zero).
+        {
+            uint4 *vs = reinterpret_cast<uint4 *>(lds + L::V_OFF);
 #pragma unroll
-            for (int c = 0; c < MS / 4; ++c) row[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int i = 0; i < Reads::VQN; ++i) vs[tid + THREADS * i] = rd.vq[i];
         }
-        if (lane < N) {
+        __syncthreads();
+        // V at the accumulator positions of P_K (bf16 held two to a register);
+        // read before the gram overwrites the staging area.
+        using VT = typename std::conditional<F32IN, float, bf16x2>::type;
+        constexpr int VPER = F32IN ? 1 : 2;
+        VT vr[MT][16 / VPER];
+        {
+            const In *vs = reinterpret_cast<const In *>(lds + L::V_OFF);
+#pragma unroll
+            for (int m = 0; m < MT; ++m)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const In x = vs[(32 * m + acc_row(r, hg)) * D + col];
+                    if constexpr (F32IN)
+                        vr[m][r] = x;
+                    else
+                        vr[m][r >> 1][r & 1] = x;
+                }
+        }
+        __syncthreads();
+
+        // ---- phase 2: masked, decay-weighted gram tiles (lower triangle) --
+        //   B[t,i] = beta_t (g_t/g_i) (k_t . k_i)  for i a strict ancestor of t
+        //   A[t,i] = (g_t/g_i) (q_t . k_i)          for i ancestor-or-self of t
+        // Every entry of B and A is written: the upper tile as zeros.
+        constexpr int NPAIRS = MT * (MT + 1) / 2;
+        if (wave < NPAIRS) {
+            const int mt = wave == 0 ? 0 : 1;
+            const int nt = wave == 2 ? 1 : 0;
+            f32x16 gkk = {}, gqk = {};
+            const __bf16 *ak_row = Xh + (32 * mt + l32) * XS + 8 * hg;
+            const __bf16 *aq_row = Xh + (NP + 32 * mt + l32) * XS + 8 * hg;
+            const __bf16 *bk_row = Xh + (32 * nt + l32) * XS + 8 * hg;
+#pragma unroll 2
+            for (int s = 0; s < 8; ++s) {
+                const bf16x8 ak = *reinterpret_cast<const bf16x8 *>(ak_row + 16 * s);
+                const bf16x8 aq = *reinterpret_cast<const bf16x8 *>(aq_row + 16 * s);
+                const bf16x8 bk = *reinterpret_cast<const bf16x8 *>(bk_row + 16 * s);
+                gkk = mma(ak, bk, gkk);
+                gqk = mma(aq, bk, gqk);
+                if constexpr (F32IN) {
+                    const ptrdiff_t lo = Xl - Xh;
+                    const bf16x8 akl = *reinterpret_cast<const bf16x8 *>(ak_row + lo + 16 * s);
+                    const bf16x8 aql = *reinterpret_cast<const bf16x8 *>(aq_row + lo + 16 * s);
+                    const bf16x8 bkl = *reinterpret_cast<const bf16x8 *>(bk_row + lo + 16 * s);
+                    gkk = mma(ak, bkl, gkk);
+                    gkk = mma(akl, bk, gkk);
+                    gqk = mma(aq, bkl, gqk);
+                    gqk = mma(aql, bk, gqk);
+                }
+            }
+            const int ci = 32 * nt + l32;
+            const float inv_gi = 1.f / g_s[ci];
+#pragma unroll
+            for (int r4 = 0; r4 < 16; r4 += 4) {             // four consecutive rows at a time
+#pragma unroll
+                for (int r = r4; r < r4 + 4; ++r) {
+                    const int t = 32 * mt + acc_row(r, hg);
+                    const bool strict = (anc_s[t] >> ci) & 1ull;
+                    const float ratio = strict ? g_s[t] * inv_gi : (ci == t ? 1.f : 0.f);
+                    Bm[t * MS + ci] = strict ? be_s[t] * ratio * gkk[r] : 0.f;
+                    Am[t * MS + ci] = ratio * gqk[r];
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        } else if (MT == 2 && wave == 3) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int t = acc_row(r, hg);
+                Bm[t * MS + 32 + l32] = 0.f;
+                Am[t * MS + 32 + l32] = 0.f;
+            }
+        }
+
+        // ---- phase 3: P = [K; Q] S0^T for this wave's 32 columns ----------
+        // The A operands (rows of [K; Q] in LDS) are double-buffered one
+        // K-step ahead; the scheduling barriers keep the compiler from
+        // hoisting every step's operands at once.
+        f32x16 accp[2 * MT];
+#pragma unroll
+        for (int m = 0; m < 2 * MT; ++m) accp[m] = f32x16{};
+        {
+            bf16x8 afr[2][2 * MT], alo[2][2 * MT];
+            auto load_a = [&](int buf, int s) {
+#pragma unroll
+                for (int m = 0; m < 2 * MT; ++m) {
+                    const __bf16 *arow = Xh + (32 * m + l32) * XS + 16 * s + 8 * hg;
+                    afr[buf][m] = *reinterpret_cast<const bf16x8 *>(arow);
+                    if constexpr (F32IN) alo[buf][m] = *reinterpret_cast<const bf16x8 *>(arow + (Xl - Xh));
+                }
+            };
+            load_a(0, 0);
+#pragma unroll
+            for (int s = 0; s < 8; ++s) {
+                if (s < 7) load_a((s + 1) & 1, s + 1);
+                float sv[8];
+                *reinterpret_cast<f32x4 *>(sv) = rd.s0[s][0];
+                *reinterpret_cast<f32x4 *>(sv + 4) = rd.s0[s][1];
+                bf16x8 bh, bl;
+                split8(sv, bh, bl);
+#pragma unroll
+                for (int m = 0; m < 2 * MT; ++m) {
+                    accp[m] = mma(afr[s & 1][m], bh, accp[m]);
+                    accp[m] = mma(afr[s & 1][m], bl, accp[m]);
+                    if constexpr (F32IN) accp[m] = mma(alo[s & 1][m], bh, accp[m]);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        __syncthreads();
+
+        // ---- phase 4: rows of T = (I + B)^{-1} (wave 0); R and g P_Q (all) -
+        // (T (I + B))[t, j] = 0 for j != t gives, walking t's ancestors j from
+        // the nearest upwards, T[t, j] = -sum over i in {t} and the ancestors
+        // of t below j of T[t, i] B[i, j], with T[t, t] = 1.
+        if (wave == 0 && lane < NP) {
             const int t = lane;
             float *Tt = Tm + t * MS;
-            Tt[t] = 1.f;
-            const uint64_t anc = anc_s[t];
-            uint64_t rem = anc;
-            while (rem) {
-                const int j = 63 - __builtin_clzll(rem);
-                rem &= ~(1ull << j);
-                float acc = Bm[t * MS + j];
-                uint64_t below = anc & ~((2ull << j) - 1ull);   // ancestors of t deeper than j
-                while (below) {
-                    const int i = __builtin_ctzll(below);
-                    below &= below - 1;
-                    acc += Tt[i] * Bm[i * MS + j];
+            {
+                f32x4 *row = reinterpret_cast<f32x4 *>(Tt);
+#pragma unroll
+                for (int c = 0; c < MS / 4; ++c) row[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+            }
+            const uint64_t anc = t < N ? anc_s[t] : 0ull;
+            if (t < N) Tt[t] = 1.f;
+            constexpr int FAST = 8;                      // ancestors held in registers
+            if (!__any(__popcll(anc) > FAST)) {
+                int a[FAST];                             // a[0] = parent(t), a[1] = its parent, ...
+                uint64_t rem = anc;
+#pragma unroll
+                for (int kk = 0; kk < FAST; ++kk) {
+                    a[kk] = rem ? 63 - __builtin_clzll(rem) : t;
+                    rem &= ~(1ull << (a[kk] & 63));
                 }
-                Tt[j] = -acc;
+                const int m = __popcll(anc);
+                float bt[FAST], bb[FAST][FAST], x[FAST];
+#pragma unroll
+                for (int kk = 0; kk < FAST; ++kk) {
+                    bt[kk] = kk < m ? Bm[t * MS + a[kk]] : 0.f;
+#pragma unroll
+                    for (int l = 0; l < kk; ++l) bb[l][kk] = kk < m ? Bm[a[l] * MS + a[kk]] : 0.f;
+                }
+#pragma unroll
+                for (int kk = 0; kk < FAST; ++kk) {
+                    float acc = bt[kk];
+#pragma unroll
+                    for (int l = 0; l < kk; ++l) acc += x[l] * bb[l][kk];
+                    x[kk] = -acc;
+                }
+#pragma unroll
+                for (int kk = 0; kk < FAST; ++kk)
+                    if (kk < m) Tt[a[kk]] = x[kk];
+            } else if (t < N) {
+                uint64_t rem = anc;
+                while (rem) {
+                    const int j = 63 - __builtin_clzll(rem);
+                    rem &= ~(1ull << j);
+                    float acc = Bm[t * MS + j];
+                    uint64_t below = anc & ~((2ull << j) - 1ull);   // ancestors of t deeper than j
+                    while (below) {
+                        const int i = __builtin_ctzll(below);
+                        below &= below - 1;
+                        acc += Tt[i] * Bm[i * MS + j];
+                    }
+                    Tt[j] = -acc;
+                }
             }
         }
-    }
 #pragma unroll
-    for (int m = 0; m < MT; ++m)
+        for (int m = 0; m < MT; ++m)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int t = 32 * m + acc_row(r, hg);
-            const float gt = g_s[t];
-            accp[m][r] = be_s[t] * (vr[m][r] - gt * accp[m][r]);
-            accp[MT + m][r] *= gt;
-        }
-    __syncthreads();
+            for (int r = 0; r < 16; ++r) {
+                const int t = 32 * m + acc_row(r, hg);
+                const float gt = g_s[t];
+                float vt;
+                if constexpr (F32IN)
+                    vt = vr[m][r];
+                else
+                    vt = (float)vr[m][r >> 1][r & 1];
+                accp[m][r] = be_s[t] * (vt - gt * accp[m][r]);
+                accp[MT + m][r] *= gt;
+            }
+        __syncthreads();
 
-    // ---- phase 5: U = T R, then O = g P_Q + A U ---------------------------
-    // K-step s covers nodes [16s, 16s+16) in the order the accumulator holds
-    // them: slot e of lane group hg is node 32(s/2) + 16(s%2) + 8(e/4) + 4hg + e%4.
-    f32x16 accv[MT];
+        // ---- phase 5: U = T R, then O = g P_Q + A U ------------------------
+        // K-step s covers nodes [16s, 16s+16) in the order the accumulator
+        // holds them: slot e of lane group hg is node 32(s/2) + 16(s%2) +
+        // 8(e/4) + 4hg + e%4.
+        f32x16 accv[MT];
 #pragma unroll
-    for (int m = 0; m < MT; ++m) accv[m] = f32x16{};
+        for (int m = 0; m < MT; ++m) accv[m] = f32x16{};
 #pragma unroll
-    for (int s = 0; s < 2 * MT; ++s) {
-        const int m = s >> 1, hh = s & 1;
-        bf16x8 bh, bl;
-        split8(reinterpret_cast<const float *>(&accp[m]) + 8 * hh, bh, bl);
+        for (int s = 0; s < 2 * MT; ++s) {
+            const int m = s >> 1, hh = s & 1;
+            bf16x8 bh, bl;
+            split8(reinterpret_cast<const float *>(&accp[m]) + 8 * hh, bh, bl);
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            if (s > 2 * mt + 1) continue;                // T is zero above the diagonal blocks
-            const float *trow = Tm + (32 * mt + l32) * MS + 32 * m + 16 * hh + 4 * hg;
-            float ta[8];
-            *reinterpret_cast<f32x4 *>(ta) = *reinterpret_cast<const f32x4 *>(trow);
-            *reinterpret_cast<f32x4 *>(ta + 4) = *reinterpret_cast<const f32x4 *>(trow + 8);
-            bf16x8 ah, alo;
-            split8(ta, ah, alo);
-            accv[mt] = mma(ah, bh, accv[mt]);
-            accv[mt] = mma(ah, bl, accv[mt]);
-            accv[mt] = mma(alo, bh, accv[mt]);
+            for (int mt = 0; mt < MT; ++mt) {
+                if (s > 2 * mt + 1) continue;            // T is zero above the diagonal blocks
+                const float *trow = Tm + (32 * mt + l32) * MS + 32 * m + 16 * hh + 4 * hg;
+                float ta[8];
+                *reinterpret_cast<f32x4 *>(ta) = *reinterpret_cast<const f32x4 *>(trow);
+                *reinterpret_cast<f32x4 *>(ta + 4) = *reinterpret_cast<const f32x4 *>(trow + 8);
+                bf16x8 ah, alo;
+                split8(ta, ah, alo);
+                accv[mt] = mma(ah, bh, accv[mt]);
+                accv[mt] = mma(ah, bl, accv[mt]);
+                accv[mt] = mma(alo, bh, accv[mt]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
         }
+        __syncthreads();                                 // every wave is done reading T
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) Us[(32 * m + acc_row(r, hg)) * US + col] = accv[m][r];
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int s = 0; s < 2 * MT; ++s) {
+            const int m = s >> 1, hh = s & 1;
+            bf16x8 bh, bl;
+            split8(reinterpret_cast<const float *>(&accv[m]) + 8 * hh, bh, bl);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                if (s > 2 * mt + 1) continue;
+                const float *arow = Am + (32 * mt + l32) * MS + 32 * m + 16 * hh + 4 * hg;
+                float aa[8];
+                *reinterpret_cast<f32x4 *>(aa) = *reinterpret_cast<const f32x4 *>(arow);
+                *reinterpret_cast<f32x4 *>(aa + 4) = *reinterpret_cast<const f32x4 *>(arow + 8);
+                bf16x8 ah, alo;
+                split8(aa, ah, alo);
+                accp[MT + mt] = mma(ah, bh, accp[MT + mt]);
+                accp[MT + mt] = mma(ah, bl, accp[MT + mt]);
+                accp[MT + mt] = mma(alo, bh, accp[MT + mt]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        const rsrc_t ru = make_rsrc(U + node0 * D, N * D * 4);
+        const rsrc_t ro = make_rsrc(o + node0 * D, N * D * (int)sizeof(In));
+        if constexpr (!F32IN) {
+#pragma unroll
+            for (int m = 0; m < MT; ++m)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) Os[(32 * m + acc_row(r, hg)) * OS + col] = (__bf16)accp[MT + m][r];
+            __builtin_amdgcn_sched_barrier(0);
+        } else {
+#pragma unroll
+            for (int m = 0; m < MT; ++m)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    st_f32(ro, ((32 * m + acc_row(r, hg)) * D + col) * 4, accp[MT + m][r]);
+        }
+        __syncthreads();
+        // Whole rows out, 16 bytes per lane; rows of padding nodes fall past
+        // the end of the descriptors and are dropped.
+#pragma unroll
+        for (int it = 0; it < NP * (D / 4) / THREADS; ++it) {
+            const int idx = tid + THREADS * it, t = idx / (D / 4), c = (idx % (D / 4)) * 4;
+            st_u32x4(ru, (t * D + c) * 4, *reinterpret_cast<const uint4 *>(Us + t * US + c));
+        }
+        if constexpr (!F32IN) {
+#pragma unroll
+            for (int it = 0; it < NP * (D / 8) / THREADS; ++it) {
+                const int idx = tid + THREADS * it, t = idx / (D / 8), c = (idx % (D / 8)) * 8;
+                st_u32x4(ro, (t * D + c) * 2, *reinterpret_cast<const uint4 *>(Os + t * OS + c));
+            }
+        }
+        __syncthreads();                                 // LDS is rewritten by the next unit
     }
-#pragma unroll
-    for (int m = 0; m < MT; ++m)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int t = 32 * m + acc_row(r, hg);
-            if (t < N) U[(node0 + t) * D + col] = accv[m][r];
-        }
-#pragma unroll
-    for (int s = 0; s < 2 * MT; ++s) {
-        const int m = s >> 1, hh = s & 1;
-        bf16x8 bh, bl;
-        split8(reinterpret_cast<const float *>(&accv[m]) + 8 * hh, bh, bl);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            if (s > 2 * mt + 1) continue;
-            const float *arow = Am + (32 * mt + l32) * MS + 32 * m + 16 * hh + 4 * hg;
-            float aa[8];
-            *reinterpret_cast<f32x4 *>(aa) = *reinterpret_cast<const f32x4 *>(arow);
-            *reinterpret_cast<f32x4 *>(aa + 4) = *reinterpret_cast<const f32x4 *>(arow + 8);
-            bf16x8 ah, alo;
-            split8(aa, ah, alo);
-            accp[MT + mt] = mma(ah, bh, accp[MT + mt]);
-            accp[MT + mt] = mma(ah, bl, accp[MT + mt]);
-            accp[MT + mt] = mma(alo, bh, accp[MT + mt]);
-        }
-    }
-#pragma unroll
-    for (int m = 0; m < MT; ++m)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int t = 32 * m + acc_row(r, hg);
-            if (t < N) o[(node0 + t) * D + col] = from_f32<In>(accp[MT + m][r]);
-        }
 }
+
+namespace {
+
+template <int NP, bool F32IN>
+int resident_grid(int units) {
+    static int per_device[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+    if (per_device[dev] == 0) {
+        int cus = 0, blocks = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+            cus = 256;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, verify_kernel<NP, F32IN>, THREADS, 0) !=
+                hipSuccess || blocks <= 0)
+            blocks = 1;
+        per_device[dev] = cus * blocks;
+    }
+    return units < per_device[dev] ? units : per_device[dev];
+}
+
+template <int NP, bool F32IN>
+hipError_t launch(const float *S0, const void *q, const void *k, const void *v, const float *alpha,
+                  const float *beta, const int32_t *parent, int N, int B, int H, void *o, float *U,
+                  int32_t *err, hipStream_t stream) {
+    const int units = B * H;
+    hipLaunchKernelGGL((verify_kernel<NP, F32IN>), dim3((unsigned)resident_grid<NP, F32IN>(units)),
+                       dim3(THREADS), 0, stream, S0, q, k, v, alpha, beta, parent, N, H, units, o, U, err);
+    return hipGetLastError();
+}
+
+}  // namespace
 
 hipError_t launch_verify(const float *S0, const void *q, const void *k, const void *v,
                          const float *alpha, const float *beta, const int32_t *parent, int N,
                          int B, int H, bool f32_in, void *o, float *U, int32_t *err,
                          hipStream_t stream) {
-    const dim3 grid((unsigned)(B * H)), block(THREADS);
-    if (N <= 32) {
-        if (f32_in)
-            hipLaunchKernelGGL((verify_kernel<32, true>), grid, block, 0, stream, S0, q, k, v, alpha,
-                               beta, parent, N, H, o, U, err);
-        else
-            hipLaunchKernelGGL((verify_kernel<32, false>), grid, block, 0, stream, S0, q, k, v, alpha,
-                               beta, parent, N, H, o, U, err);
-    } else {
-        if (f32_in)
-            hipLaunchKernelGGL((verify_kernel<64, true>), grid, block, 0, stream, S0, q, k, v, alpha,
-                               beta, parent, N, H, o, U, err);
-        else
-            hipLaunchKernelGGL((verify_kernel<64, false>), grid, block, 0, stream, S0, q, k, v, alpha,
-                               beta, parent, N, H, o, U, err);
-    }
-    return hipGetLastError();
+    if (N <= 32)
+        return f32_in ? launch<32, true>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, stream)
+                      : launch<32, false>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, stream);
+    return f32_in ? launch<64, true>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, stream)
+                  : launch<64, false>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, stream);
 }
 
 }  // namespace treewy

@@ -101,14 +101,18 @@ def _rngs(cfg_key: int, seed: int) -> Dict[str, np.random.Generator]:
 def round_to_bf16(x: np.ndarray) -> np.ndarray:
     """Round float32 values to the nearest bfloat16 (ties to even); return float32."""
     x32 = np.ascontiguousarray(x, dtype=np.float32)
-    bits = x32.view(np.uint32).astype(np.uint64)
-    bits = (bits + 0x7FFF + ((bits >> 16) & 1)) & 0xFFFF0000
-    return bits.astype(np.uint32).view(np.float32).reshape(x32.shape)
+    if not np.isfinite(x32).all():
+        raise ValueError("round_to_bf16 expects finite values")
+    bits = x32.view(np.uint32)
+    out = bits + np.uint32(0x7FFF) + ((bits >> np.uint32(16)) & np.uint32(1))
+    out &= np.uint32(0xFFFF0000)
+    return out.view(np.float32).reshape(x32.shape)
 
 
-def _unit_rows(rng: np.random.Generator, shape: Tuple[int, ...]) -> np.ndarray:
-    x = rng.standard_normal(shape)
-    return x / np.linalg.norm(x, axis=-1, keepdims=True)
+def _unit_rows(rng: np.random.Generator, shape: Tuple[int, ...], dtype=np.float64) -> np.ndarray:
+    x = rng.standard_normal(shape, dtype=dtype)
+    x /= np.sqrt(np.einsum("...i,...i->...", x, x))[..., None]
+    return x
 
 
 # --------------------------------------------------------------------------
@@ -257,8 +261,8 @@ def make_inputs(w: Workload, seed: int = 0, cfg_key: Optional[int] = None) -> Di
         parents = np.tile(chain_tree(N), (B, 1))
     else:
         parents = np.stack([random_tree(r["tree"], N, w.max_depth, w.caps) for _ in range(B)])
-    q = _unit_rows(r["q"], (B, H, N, dk)).astype(np.float32)
-    k = _unit_rows(r["k"], (B, H, N, dk)).astype(np.float32)
+    q = _unit_rows(r["q"], (B, H, N, dk), np.float32)
+    k = _unit_rows(r["k"], (B, H, N, dk), np.float32)
     v = r["v"].standard_normal((B, H, N, dv), dtype=np.float32)
     if w.in_dtype == "bf16":
         q, k, v = round_to_bf16(q), round_to_bf16(k), round_to_bf16(v)
@@ -305,3 +309,23 @@ def sample_units(w: Workload, count: int, seed: int = 0) -> np.ndarray:
         return np.arange(w.units)
     pick = rng.choice(np.arange(1, w.units - 1), size=max(count - 2, 0), replace=False)
     return np.unique(np.concatenate([[0, w.units - 1], pick])).astype(np.int64)
+
+
+def warmup_chunk_torch(w: Workload, seed: int, chunk: int, T: int, device, dtype):
+    """Warm-up tokens drawn on the device with torch (for large batches).
+
+    Returns k [B, H, T, d_k] (unit rows, cast to `dtype`), v [B, H, T, d_v]
+    (`dtype`), alpha and beta [B, H, T] (float32) from the workload's ranges.
+    """
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(20961 * 1000003 + 7919 * int(seed) + int(chunk))
+    shp = (w.B, w.H, T)
+    k = torch.randn(*shp, w.d_k, generator=g, device=device, dtype=torch.float32)
+    k = k / k.norm(dim=-1, keepdim=True)
+    v = torch.randn(*shp, w.d_v, generator=g, device=device, dtype=torch.float32)
+    lo, hi = w.alpha_range
+    alpha = lo + (hi - lo) * torch.rand(*shp, generator=g, device=device, dtype=torch.float32)
+    lo, hi = w.beta_range
+    beta = lo + (hi - lo) * torch.rand(*shp, generator=g, device=device, dtype=torch.float32)
+    return k.to(dtype).contiguous(), v.to(dtype).contiguous(), alpha.contiguous(), beta.contiguous()
