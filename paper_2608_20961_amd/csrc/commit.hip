@@ -32,10 +32,11 @@ __global__ __launch_bounds__(THREADS) void commit_kernel(
     const int tid = threadIdx.x, u = blockIdx.x, b = u / H;
     const size_t node0 = (size_t)u * N;
 
-    const f32x4 *src = reinterpret_cast<const f32x4 *>(S0 + (size_t)u * D * D);
+    // The state is touched once: stream it past the caches on the way in and out.
+    const rsrc_t rs = make_rsrc(S0 + (size_t)u * D * D, D * D * 4);
     f32x4 s[16];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) s[i] = src[tid + THREADS * i];
+    for (int i = 0; i < 16; ++i) s[i] = ld_f32x4<STREAM>(rs, (tid + THREADS * i) * 16);
 
     if (tid == 0) {
         const int len = path_len[b];
@@ -81,9 +82,9 @@ __global__ __launch_bounds__(THREADS) void commit_kernel(
 #pragma unroll
         for (int i = 0; i < 16; ++i) s[i] += uw[8 * i] * kk;
     }
-    f32x4 *dst = reinterpret_cast<f32x4 *>(S_new + (size_t)u * D * D);
+    const rsrc_t rd = make_rsrc(S_new + (size_t)u * D * D, D * D * 4);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) dst[tid + THREADS * i] = s[i];
+    for (int i = 0; i < 16; ++i) st_u32x4<STREAM>(rd, (tid + THREADS * i) * 16, __builtin_bit_cast(uint4, s[i]));
 }
 
 hipError_t launch_commit(const float *S0, const float *U, const void *k, const float *alpha,

@@ -53,11 +53,19 @@ typedef __amdgpu_buffer_rsrc_t rsrc_t;
 __device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
 }
-__device__ __forceinline__ f32x4 ld_f32x4(rsrc_t r, int off) {
-    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+
+// Cache policy of a buffer access.  STREAM sets the non-temporal bit: the line
+// is not kept in L2 / MALL after use, which suits data each kernel touches
+// once (the state, the node vectors, U and o) and lets a read+write stream
+// run closer to the HBM rate than the default write-back policy does.
+constexpr int CACHED = 0;
+constexpr int STREAM = 2;
+
+template <int P = CACHED> __device__ __forceinline__ f32x4 ld_f32x4(rsrc_t r, int off) {
+    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, P));
 }
-__device__ __forceinline__ uint4 ld_u32x4(rsrc_t r, int off) {
-    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+template <int P = CACHED> __device__ __forceinline__ uint4 ld_u32x4(rsrc_t r, int off) {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, P));
 }
 __device__ __forceinline__ float ld_f32(rsrc_t r, int off) {
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
@@ -71,12 +79,12 @@ __device__ __forceinline__ __bf16 ld_bf16(rsrc_t r, int off) {
 template <typename T> __device__ __forceinline__ T ld_elem(rsrc_t r, int off);
 template <> __device__ __forceinline__ float ld_elem<float>(rsrc_t r, int off) { return ld_f32(r, off); }
 template <> __device__ __forceinline__ __bf16 ld_elem<__bf16>(rsrc_t r, int off) { return ld_bf16(r, off); }
-__device__ __forceinline__ void st_u32x4(rsrc_t r, int off, uint4 x) {
+template <int P = CACHED> __device__ __forceinline__ void st_u32x4(rsrc_t r, int off, uint4 x) {
     __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned int, x),
-                                           r, off, 0, 0);
+                                           r, off, 0, P);
 }
-__device__ __forceinline__ void st_f32(rsrc_t r, int off, float x) {
-    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned int, x), r, off, 0, 0);
+template <int P = CACHED> __device__ __forceinline__ void st_f32(rsrc_t r, int off, float x) {
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned int, x), r, off, 0, P);
 }
 
 // A copy of x the compiler cannot see through (keeps derived values inside a loop).

@@ -16,7 +16,8 @@
 // core operand registers.  K and Q are staged once in LDS as bf16 and read by
 // all four waves.  T = (I + B)^{-1} has the ancestor sparsity of the tree, and
 // row t of T only involves the entries of B between t's ancestors, so each
-// lane of wave 0 builds one row of T independently (work ~ depth^2).  U = T R
+// lane of one wave builds one row of T independently (work ~ depth^2), in
+// place over B while the other waves start on P.  U = T R
 // and A U then run on the matrix cores with R and U taken straight from the
 // accumulator registers (the contraction index is permuted to match the
 // accumulator layout; T and A are read in the same permuted order).  U and O
@@ -25,7 +26,10 @@
 // Streaming.  All of a unit's HBM reads are issued at once, in the order they
 // are consumed (tree and gates, K/Q, V, then S0), through buffer descriptors
 // bounded to the unit so padding rows read as zero without branches; two
-// workgroups per CU keep HBM busy while the other one computes.
+// workgroups per CU keep HBM busy while the other one computes.  K/Q/V loads
+// and U/o stores cover whole cache lines per instruction and go out
+// non-temporal; S0's operand-layout loads reach each line through four
+// instructions and keep the default policy so the line stays in L2 between them.
 //
 // Precision.  The matrix cores take bf16; fp32 operands are split into
 // hi + lo bf16 pairs and multiplied in three passes (hi*hi + hi*lo + lo*hi),
@@ -50,7 +54,8 @@ struct VerifyLds {
     static constexpr int BETA_OFF = A_OFF + M_BYTES;
     static constexpr int G_OFF = BETA_OFF + NP * 4;
     static constexpr int ANC_OFF = G_OFF + NP * 4;
-    static constexpr int END = ANC_OFF + NP * 8;
+    static constexpr int FLAG_OFF = ANC_OFF + NP * 8;   // 1 when every node has <= FAST ancestors
+    static constexpr int END = FLAG_OFF + 16;
     static constexpr bool O_IN_B = NP * OS * 2 <= M_BYTES;   // o staged where B was, else appended
     static constexpr int O_OFF = O_IN_B ? B_OFF : END;
     static constexpr int END_O = (O_IN_B || F32IN) ? END : END + NP * OS * 2;
@@ -60,7 +65,8 @@ struct VerifyLds {
     static constexpr int BYTES = V_IN_BA ? END_O : END_O + V_BYTES;
     static_assert(NP * MS * 4 <= X_BYTES, "T must fit where K/Q were staged");
     static_assert(NP * US * 4 <= B_OFF, "U staging must fit where K/Q were staged");
-    static_assert(B_OFF % 16 == 0 && A_OFF % 16 == 0 && ANC_OFF % 8 == 0 && O_OFF % 16 == 0 &&
+    static_assert(B_OFF % 16 == 0 && A_OFF % 16 == 0 && BETA_OFF % 16 == 0 && G_OFF % 16 == 0 &&
+                  ANC_OFF % 32 == 0 && O_OFF % 16 == 0 &&
                   V_OFF % 16 == 0, "alignment");
 };
 
@@ -99,17 +105,17 @@ struct UnitReads {
         for (int i = 0; i < KQN; ++i) {
             const int idx = tid + THREADS * i, r = idx / CPR, c = (idx % CPR) * CHUNK;
             const int t = i < KN ? r : r - NP;
-            kq[i] = ld_u32x4(i < KN ? rk : rq, t * ROW + c * (int)sizeof(In));
+            kq[i] = ld_u32x4<STREAM>(i < KN ? rk : rq, t * ROW + c * (int)sizeof(In));
         }
         const rsrc_t rv = make_rsrc(vv + node0 * D, N * ROW);
 #pragma unroll
-        for (int i = 0; i < VQN; ++i) vq[i] = ld_u32x4(rv, (tid + THREADS * i) * 16);
+        for (int i = 0; i < VQN; ++i) vq[i] = ld_u32x4<STREAM>(rv, (tid + THREADS * i) * 16);
         const rsrc_t rs = make_rsrc(S0 + (size_t)u * D * D, D * D * 4);
         const int base = (col * D + 8 * hg) * 4;
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
-            s0[s][0] = ld_f32x4(rs, base + 64 * s);
-            s0[s][1] = ld_f32x4(rs, base + 64 * s + 16);
+            s0[s][0] = ld_f32x4<CACHED>(rs, base + 64 * s);
+            s0[s][1] = ld_f32x4<CACHED>(rs, base + 64 * s + 16);
         }
     }
 };
@@ -132,12 +138,14 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
     __bf16 *Xl = reinterpret_cast<__bf16 *>(lds + L::XLO_OFF);
     float *Bm = reinterpret_cast<float *>(lds + L::B_OFF);
     float *Am = reinterpret_cast<float *>(lds + L::A_OFF);
-    float *Tm = reinterpret_cast<float *>(lds);          // T reuses the K/Q area once P is done,
+    float *Tm = reinterpret_cast<float *>(lds);          // T of deep trees reuses the K/Q area after P,
     float *Us = reinterpret_cast<float *>(lds);          // then U is staged there
     __bf16 *Os = reinterpret_cast<__bf16 *>(lds + L::O_OFF);   // o staging (bf16 input only)
     float *be_s = reinterpret_cast<float *>(lds + L::BETA_OFF);
     float *g_s = reinterpret_cast<float *>(lds + L::G_OFF);
     uint64_t *anc_s = reinterpret_cast<uint64_t *>(lds + L::ANC_OFF);
+    int *shallow_s = reinterpret_cast<int *>(lds + L::FLAG_OFF);
+    constexpr int FAST = 8;                              // ancestors a lane holds in registers
 
     const In *q = static_cast<const In *>(q_);
     const In *k = static_cast<const In *>(k_);
@@ -189,6 +197,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 be_s[lane] = lane < N ? rd.be : 0.f;
                 anc_s[lane] = mask;
             }
+            const bool shallow = !__any(__popcll(mask) > FAST);
+            if (lane == 0) *shallow_s = shallow ? 1 : 0;
         }
         // K and Q into LDS as bf16 (hi/lo for fp32 input), padding rows zero.
 #pragma unroll
@@ -268,17 +278,26 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             }
             const int ci = 32 * nt + l32;
             const float inv_gi = 1.f / g_s[ci];
+            // The accumulator rows come in runs of four consecutive nodes, so
+            // their decays, betas and ancestor masks arrive as 16-byte LDS
+            // broadcasts; bit ci of a mask sits in word nt of the row's u64.
 #pragma unroll
-            for (int r4 = 0; r4 < 16; r4 += 4) {             // four consecutive rows at a time
+            for (int r4 = 0; r4 < 16; r4 += 4) {
+                const int t0 = 32 * mt + acc_row(r4, hg);      // rows t0 .. t0 + 3
+                const f32x4 g4 = *reinterpret_cast<const f32x4 *>(g_s + t0);
+                const f32x4 b4 = *reinterpret_cast<const f32x4 *>(be_s + t0);
+                const uint4 m01 = *reinterpret_cast<const uint4 *>(anc_s + t0);
+                const uint4 m23 = *reinterpret_cast<const uint4 *>(anc_s + t0 + 2);
+                const uint32_t w[4] = {nt ? m01.y : m01.x, nt ? m01.w : m01.z,
+                                       nt ? m23.y : m23.x, nt ? m23.w : m23.z};
 #pragma unroll
-                for (int r = r4; r < r4 + 4; ++r) {
-                    const int t = 32 * mt + acc_row(r, hg);
-                    const bool strict = (anc_s[t] >> ci) & 1ull;
-                    const float ratio = strict ? g_s[t] * inv_gi : (ci == t ? 1.f : 0.f);
-                    Bm[t * MS + ci] = strict ? be_s[t] * ratio * gkk[r] : 0.f;
+                for (int e = 0; e < 4; ++e) {
+                    const int r = r4 + e, t = t0 + e;
+                    const bool strict = (w[e] >> l32) & 1u;
+                    const float ratio = strict ? g4[e] * inv_gi : (ci == t ? 1.f : 0.f);
+                    Bm[t * MS + ci] = strict ? b4[e] * ratio * gkk[r] : 0.f;
                     Am[t * MS + ci] = ratio * gqk[r];
                 }
-                __builtin_amdgcn_sched_barrier(0);
             }
         } else if (MT == 2 && wave == 3) {
 #pragma unroll
@@ -287,6 +306,47 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 Bm[t * MS + 32 + l32] = 0.f;
                 Am[t * MS + 32 + l32] = 0.f;
             }
+        }
+
+        __syncthreads();
+        const bool shallow = *shallow_s != 0;
+        // ---- phase 3a: rows of T = (I + B)^{-1} for shallow trees ----------
+        // (T (I + B))[t, j] = 0 for j != t gives, walking t's ancestors j from
+        // the nearest upwards, T[t, j] = -sum over i in {t} and the ancestors
+        // of t below j of T[t, i] B[i, j], with T[t, t] = 1.  T has the
+        // sparsity of B plus the diagonal, so with every entry a lane needs
+        // gathered into registers first, row t of T overwrites row t of B.
+        // One wave does it while the others start on P.
+        if (shallow && wave == 3 && lane < NP) {
+            const int t = lane;
+            const uint64_t anc = t < N ? anc_s[t] : 0ull;
+            int a[FAST];                                 // a[0] = parent(t), a[1] = its parent, ...
+            uint64_t rem = anc;
+#pragma unroll
+            for (int kk = 0; kk < FAST; ++kk) {
+                a[kk] = rem ? 63 - __builtin_clzll(rem) : t;
+                rem &= ~(1ull << (a[kk] & 63));
+            }
+            const int m = __popcll(anc);
+            float bt[FAST], bb[FAST][FAST], x[FAST];
+#pragma unroll
+            for (int kk = 0; kk < FAST; ++kk) {
+                bt[kk] = kk < m ? Bm[t * MS + a[kk]] : 0.f;
+#pragma unroll
+                for (int l = 0; l < kk; ++l) bb[l][kk] = kk < m ? Bm[a[l] * MS + a[kk]] : 0.f;
+            }
+#pragma unroll
+            for (int kk = 0; kk < FAST; ++kk) {
+                float acc = bt[kk];
+#pragma unroll
+                for (int l = 0; l < kk; ++l) acc += x[l] * bb[l][kk];
+                x[kk] = -acc;
+            }
+            float *Tt = Bm + t * MS;
+            if (t < N) Tt[t] = 1.f;
+#pragma unroll
+            for (int kk = 0; kk < FAST; ++kk)
+                if (kk < m) Tt[a[kk]] = x[kk];
         }
 
         // ---- phase 3: P = [K; Q] S0^T for this wave's 32 columns ----------
@@ -326,11 +386,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         }
         __syncthreads();
 
-        // ---- phase 4: rows of T = (I + B)^{-1} (wave 0); R and g P_Q (all) -
-        // (T (I + B))[t, j] = 0 for j != t gives, walking t's ancestors j from
-        // the nearest upwards, T[t, j] = -sum over i in {t} and the ancestors
-        // of t below j of T[t, i] B[i, j], with T[t, t] = 1.
-        if (wave == 0 && lane < NP) {
+        // ---- phase 4: deep trees build T where K/Q were (wave 0); R and g P_Q
+        if (!shallow && wave == 0 && lane < NP) {
             const int t = lane;
             float *Tt = Tm + t * MS;
             {
@@ -338,36 +395,9 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 #pragma unroll
                 for (int c = 0; c < MS / 4; ++c) row[c] = f32x4{0.f, 0.f, 0.f, 0.f};
             }
-            const uint64_t anc = t < N ? anc_s[t] : 0ull;
-            if (t < N) Tt[t] = 1.f;
-            constexpr int FAST = 8;                      // ancestors held in registers
-            if (!__any(__popcll(anc) > FAST)) {
-                int a[FAST];                             // a[0] = parent(t), a[1] = its parent, ...
-                uint64_t rem = anc;
-#pragma unroll
-                for (int kk = 0; kk < FAST; ++kk) {
-                    a[kk] = rem ? 63 - __builtin_clzll(rem) : t;
-                    rem &= ~(1ull << (a[kk] & 63));
-                }
-                const int m = __popcll(anc);
-                float bt[FAST], bb[FAST][FAST], x[FAST];
-#pragma unroll
-                for (int kk = 0; kk < FAST; ++kk) {
-                    bt[kk] = kk < m ? Bm[t * MS + a[kk]] : 0.f;
-#pragma unroll
-                    for (int l = 0; l < kk; ++l) bb[l][kk] = kk < m ? Bm[a[l] * MS + a[kk]] : 0.f;
-                }
-#pragma unroll
-                for (int kk = 0; kk < FAST; ++kk) {
-                    float acc = bt[kk];
-#pragma unroll
-                    for (int l = 0; l < kk; ++l) acc += x[l] * bb[l][kk];
-                    x[kk] = -acc;
-                }
-#pragma unroll
-                for (int kk = 0; kk < FAST; ++kk)
-                    if (kk < m) Tt[a[kk]] = x[kk];
-            } else if (t < N) {
+            if (t < N) {
+                Tt[t] = 1.f;
+                const uint64_t anc = anc_s[t];
                 uint64_t rem = anc;
                 while (rem) {
                     const int j = 63 - __builtin_clzll(rem);
@@ -403,6 +433,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // K-step s covers nodes [16s, 16s+16) in the order the accumulator
         // holds them: slot e of lane group hg is node 32(s/2) + 16(s%2) +
         // 8(e/4) + 4hg + e%4.
+        const float *Tsrc = shallow ? Bm : Tm;
         f32x16 accv[MT];
 #pragma unroll
         for (int m = 0; m < MT; ++m) accv[m] = f32x16{};
@@ -414,7 +445,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
                 if (s > 2 * mt + 1) continue;            // T is zero above the diagonal blocks
-                const float *trow = Tm + (32 * mt + l32) * MS + 32 * m + 16 * hh + 4 * hg;
+                const float *trow = Tsrc + (32 * mt + l32) * MS + 32 * m + 16 * hh + 4 * hg;
                 float ta[8];
                 *reinterpret_cast<f32x4 *>(ta) = *reinterpret_cast<const f32x4 *>(trow);
                 *reinterpret_cast<f32x4 *>(ta + 4) = *reinterpret_cast<const f32x4 *>(trow + 8);
@@ -427,11 +458,20 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             __builtin_amdgcn_sched_barrier(0);
         }
         __syncthreads();                                 // every wave is done reading T
+        const rsrc_t ru = make_rsrc(U + node0 * D, N * D * 4);
+        const rsrc_t ro = make_rsrc(o + node0 * D, N * D * (int)sizeof(In));
 #pragma unroll
         for (int m = 0; m < MT; ++m)
 #pragma unroll
             for (int r = 0; r < 16; ++r) Us[(32 * m + acc_row(r, hg)) * US + col] = accv[m][r];
-        __builtin_amdgcn_sched_barrier(0);
+        __syncthreads();
+        // U leaves as whole rows, 16 bytes per lane (rows of padding nodes fall
+        // past the end of the descriptor and are dropped) while A U runs.
+#pragma unroll
+        for (int it = 0; it < NP * (D / 4) / THREADS; ++it) {
+            const int idx = tid + THREADS * it, t = idx / (D / 4), c = (idx % (D / 4)) * 4;
+            st_u32x4<STREAM>(ru, (t * D + c) * 4, *reinterpret_cast<const uint4 *>(Us + t * US + c));
+        }
 #pragma unroll
         for (int s = 0; s < 2 * MT; ++s) {
             const int m = s >> 1, hh = s & 1;
@@ -452,35 +492,23 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             }
             __builtin_amdgcn_sched_barrier(0);
         }
-        const rsrc_t ru = make_rsrc(U + node0 * D, N * D * 4);
-        const rsrc_t ro = make_rsrc(o + node0 * D, N * D * (int)sizeof(In));
         if constexpr (!F32IN) {
 #pragma unroll
             for (int m = 0; m < MT; ++m)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) Os[(32 * m + acc_row(r, hg)) * OS + col] = (__bf16)accp[MT + m][r];
-            __builtin_amdgcn_sched_barrier(0);
+            __syncthreads();
+#pragma unroll
+            for (int it = 0; it < NP * (D / 8) / THREADS; ++it) {
+                const int idx = tid + THREADS * it, t = idx / (D / 8), c = (idx % (D / 8)) * 8;
+                st_u32x4<STREAM>(ro, (t * D + c) * 2, *reinterpret_cast<const uint4 *>(Os + t * OS + c));
+            }
         } else {
 #pragma unroll
             for (int m = 0; m < MT; ++m)
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
-                    st_f32(ro, ((32 * m + acc_row(r, hg)) * D + col) * 4, accp[MT + m][r]);
-        }
-        __syncthreads();
-        // Whole rows out, 16 bytes per lane; rows of padding nodes fall past
-        // the end of the descriptors and are dropped.
-#pragma unroll
-        for (int it = 0; it < NP * (D / 4) / THREADS; ++it) {
-            const int idx = tid + THREADS * it, t = idx / (D / 4), c = (idx % (D / 4)) * 4;
-            st_u32x4(ru, (t * D + c) * 4, *reinterpret_cast<const uint4 *>(Us + t * US + c));
-        }
-        if constexpr (!F32IN) {
-#pragma unroll
-            for (int it = 0; it < NP * (D / 8) / THREADS; ++it) {
-                const int idx = tid + THREADS * it, t = idx / (D / 8), c = (idx % (D / 8)) * 8;
-                st_u32x4(ro, (t * D + c) * 2, *reinterpret_cast<const uint4 *>(Os + t * OS + c));
-            }
+                    st_f32<STREAM>(ro, ((32 * m + acc_row(r, hg)) * D + col) * 4, accp[MT + m][r]);
         }
         __syncthreads();                                 // LDS is rewritten by the next unit
     }
