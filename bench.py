@@ -283,6 +283,26 @@ def main():
         "commit": dict(rf_commit, pct_hbm_peak=round(100 * rf_commit["frac"], 2)),
         "kernel_source_hash": src_hash,
     }
+    # Fused: the previous round's commit inside this round's verify
+    # (treewy_commit_verify).  The previous round is this round's own draft
+    # and paths, so one launch moves commit + verify bytes minus one read of
+    # the state.
+    S_fused = torch.empty_like(d["S0"])
+    o_f, U_f = torch.empty_like(o), torch.empty_like(U)
+
+    def fused():
+        tw.treewy_commit_verify(S0_commit, U, d["k"], d["alpha"], d["path"], d["path_len"], d["q"], d["k"], d["v"],
+                                d["alpha"], d["beta"], d["parent"], parent_prev=d["parent"], S_new=S_fused, o=o_f,
+                                U=U_f)
+
+    _, (ms_fused,) = time_steps(torch, [fused], args.steps, args.warmup)
+    log("fused commit+verify: %.4f ms/launch" % ms_fused)
+    fb = acc.commit_verify_bytes(w, x["path_len"])
+    result["fused_commit_verify"] = dict(
+        roofline(fb, ms_fused, load_traffic("commit_verify", w.name, src_hash)),
+        kernel="treewy_commit_verify", nodes_per_s=round(nodes / (ms_fused * 1e-3), 1),
+        speedup_vs_separate_calls=round(ms_step / ms_fused, 3))
+    del S_fused, o_f, U_f
     spec = acc.speculative_state_bytes(w)
     result["speculative_state_bytes"] = {"treewy_U": spec["treewy_U"], "treewy_U_k_alpha": spec["treewy_U_k_alpha"],
                                          "snapshot_states": spec["snapshot_states"]}

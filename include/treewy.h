@@ -104,6 +104,39 @@ treewy_status treewy_commit(const float *S0, const float *U, const void *k, cons
                             treewy_dtype k_dtype, float *S_new, int32_t *err, void *stream);
 
 /*
+ * treewy_commit_verify - the previous round's commit fused into this round's
+ * verify (deferred state write).  The paper's chain kernel verifies and
+ * commits in one fused kernel (Implementation), and its Conclusion and the
+ * ReplaySSM comparison (appendix) name deferring the state write as the next
+ * lever.  Per unit this computes exactly
+ *   S_new = treewy_commit(S_old, U_prev, k_prev, alpha_prev, path)   (eq. 3)
+ *   (o, U) = treewy_verify(S_new, q, k, v, alpha, beta, parent)      (eq. 2)
+ * but reads the state once: S_new is formed in registers, written, and used
+ * as this round's S0 without a second read.
+ *
+ *   S_old      [B, H, d_v, d_k] float32    committed state before the previous round
+ *   U_prev     [B, H, N_prev, d_v] float32 the previous round's pseudo-values
+ *   k_prev     [B, H, N_prev, d_k] in_dtype its keys
+ *   alpha_prev [B, H, N_prev] float32      its decay gates
+ *   path, path_len, L_max                  its accepted paths, as for treewy_commit
+ *   parent_prev [B, N_prev] int32 or NULL  its tree, to check the paths
+ *   q, k, v, alpha, beta, parent, N        this round's draft, as for treewy_verify
+ *   S_new      [B, H, d_v, d_k] float32    written; may be the same buffer as S_old
+ *   o, U                                    written, as for treewy_verify
+ *   err        [B] int32 or NULL           BAD_PATH (that sequence's S_new = S_old) | BAD_PARENT
+ * 0 <= N_prev <= 64.  U may be the same buffer as U_prev only when N == N_prev;
+ * no other output may overlap an input.  N == 0 still commits (S_new is
+ * written, o and U are empty).
+ */
+treewy_status treewy_commit_verify(const float *S_old, const float *U_prev, const void *k_prev,
+                                   const float *alpha_prev, const int32_t *path,
+                                   const int32_t *path_len, int L_max, const int32_t *parent_prev,
+                                   int N_prev, const void *q, const void *k, const void *v,
+                                   const float *alpha, const float *beta, const int32_t *parent,
+                                   int N, int B, int H, int d_k, int d_v, treewy_dtype in_dtype,
+                                   float *S_new, void *o, float *U, int32_t *err, void *stream);
+
+/*
  * treewy_snapshot_verify - full-state-snapshotting baseline (Section "The
  * memory problem", approach (i)): runs eq. 1 node by node and writes every
  * node's full state, so that commit is a copy of one snapshot.  Same inputs

@@ -79,6 +79,13 @@ def commit_bytes(w: Workload, path_len: np.ndarray) -> int:
     return int(per_seq.sum())
 
 
+def commit_verify_bytes(w: Workload, path_len: np.ndarray) -> int:
+    """The previous round's commit fused into this round's verify (both rounds
+    shaped like `w`): commit + verify minus the second read of the state,
+    which the fused call takes from registers."""
+    return verify_bytes(w) + commit_bytes(w, path_len) - w.units * w.d_k * w.d_v * 4
+
+
 def snapshot_verify_bytes(w: Workload) -> int:
     s, d, N = elem_bytes(w.in_dtype), w.d_k, w.N
     per_unit = d * d * 4 + 3 * N * d * s + 2 * N * 4 + N * d * s + N * d * d * 4

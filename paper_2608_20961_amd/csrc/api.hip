@@ -61,6 +61,34 @@ treewy_status treewy_commit(const float *S0, const float *U, const void *k, cons
                                             static_cast<hipStream_t>(stream)));
 }
 
+treewy_status treewy_commit_verify(const float *S_old, const float *U_prev, const void *k_prev,
+                                   const float *alpha_prev, const int32_t *path,
+                                   const int32_t *path_len, int L_max, const int32_t *parent_prev,
+                                   int N_prev, const void *q, const void *k, const void *v,
+                                   const float *alpha, const float *beta, const int32_t *parent,
+                                   int N, int B, int H, int d_k, int d_v, treewy_dtype in_dtype,
+                                   float *S_new, void *o, float *U, int32_t *err, void *stream) {
+    treewy_status st = check_common(N, B, H, d_k, d_v, in_dtype);
+    if (st != TREEWY_OK) return st;
+    if (N_prev < 0 || L_max < 0) return TREEWY_ERR_INVALID_ARG;
+    if (N_prev > kMaxN || L_max > kMaxN) return TREEWY_ERR_UNSUPPORTED;
+    if (B == 0 || H == 0) return TREEWY_OK;
+    if (!S_old || !path_len || !S_new) return TREEWY_ERR_INVALID_ARG;
+    if (N_prev > 0 && (!U_prev || !k_prev || !alpha_prev)) return TREEWY_ERR_INVALID_ARG;
+    if (L_max > 0 && !path) return TREEWY_ERR_INVALID_ARG;
+    if (N > 0 && (!q || !k || !v || !alpha || !beta || !parent || !o || !U)) return TREEWY_ERR_INVALID_ARG;
+    if (!aligned16(S_old) || !aligned16(S_new) || !aligned16(U_prev) || !aligned16(k_prev) ||
+        !aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(U))
+        return TREEWY_ERR_INVALID_ARG;
+    // U over U_prev is safe only row block for row block (each unit reads its
+    // previous rows before it writes its new ones).
+    if (N > 0 && U == U_prev && N != N_prev) return TREEWY_ERR_INVALID_ARG;
+    return hip_status(treewy::launch_commit_verify(S_old, U_prev, k_prev, alpha_prev, path, path_len, L_max,
+                                                   parent_prev, N_prev, q, k, v, alpha, beta, parent, N, B,
+                                                   H, in_dtype == TREEWY_F32, S_new, o, U, err,
+                                                   static_cast<hipStream_t>(stream)));
+}
+
 treewy_status treewy_snapshot_verify(const float *S0, const void *q, const void *k, const void *v,
                                      const float *alpha, const float *beta, const int32_t *parent,
                                      int N, int B, int H, int d_k, int d_v, treewy_dtype in_dtype,

@@ -40,7 +40,20 @@
 
 namespace treewy {
 
-template <int NP, bool F32IN>
+// The previous round's accepted path, committed inside verify (fused call):
+// S0 of this round = g_a S_old + sum_l w_l U_prev[a_l] k_prev[a_l]^T.
+struct CommitArgs {
+    const float *U;           // [units, N_prev, D] pseudo-values of the previous round
+    const void *k;            // [units, N_prev, D] its keys, in the input dtype
+    const float *alpha;       // [units, N_prev]
+    const int32_t *path;      // [B, L_max] root -> accepted node
+    const int32_t *path_len;  // [B]
+    const int32_t *parent;    // [B, N_prev] or null (then only range and order are checked)
+    float *S_new;             // [units, D, D]; may be S_old
+    int L_max, N_prev;
+};
+
+template <int NP, bool F32IN, bool FUSE = false>
 struct VerifyLds {
     static constexpr int XS = D + 8;                    // bf16 per staged K/Q row (pad breaks bank aliasing)
     static constexpr int MS = NP + 4;                   // floats per row of the N x N matrices
@@ -62,18 +75,27 @@ struct VerifyLds {
     static constexpr int V_BYTES = NP * D * (F32IN ? 4 : 2);
     static constexpr bool V_IN_BA = V_BYTES <= 2 * M_BYTES;  // V staged over B and A before the gram
     static constexpr int V_OFF = V_IN_BA ? B_OFF : END_O;
-    static constexpr int BYTES = V_IN_BA ? END_O : END_O + V_BYTES;
+    static constexpr int BASE_BYTES = V_IN_BA ? END_O : END_O + V_BYTES;
+    // Fused commit: the accepted path (node, weight, then its length and g_a)
+    // in two buffers, this unit's and the next one's, and CL path rows at a
+    // time, transposed: k as [d_k][CL], w U as [d_v][CL].
+    static constexpr int CL = 8;
+    static constexpr int META_BYTES = 64 * 4 + 64 * 4 + 16;
+    static constexpr int META_OFF = BASE_BYTES;
+    static constexpr int KPT_OFF = META_OFF + 2 * META_BYTES;
+    static constexpr int UWT_OFF = KPT_OFF + D * CL * (F32IN ? 4 : 2);
+    static constexpr int BYTES = FUSE ? UWT_OFF + D * CL * 4 : BASE_BYTES;
     static_assert(NP * MS * 4 <= X_BYTES, "T must fit where K/Q were staged");
     static_assert(NP * US * 4 <= B_OFF, "U staging must fit where K/Q were staged");
     static_assert(B_OFF % 16 == 0 && A_OFF % 16 == 0 && BETA_OFF % 16 == 0 && G_OFF % 16 == 0 &&
-                  ANC_OFF % 32 == 0 && O_OFF % 16 == 0 &&
-                  V_OFF % 16 == 0, "alignment");
+                  ANC_OFF % 32 == 0 && O_OFF % 16 == 0 && V_OFF % 16 == 0 &&
+                  KPT_OFF % 16 == 0 && UWT_OFF % 16 == 0, "alignment");
 };
 
 // One unit's HBM reads, held in registers from issue to use.  Every read goes
 // through a buffer descriptor bounded to this unit's rows, so rows of padding
 // nodes (t >= N) read as zero.
-template <int NP, bool F32IN>
+template <int NP, bool F32IN, bool FUSE = false>
 struct UnitReads {
     using In = typename std::conditional<F32IN, float, __bf16>::type;
     static constexpr int MT = NP / 32;
@@ -85,9 +107,30 @@ struct UnitReads {
     int par;                                            // wave 0, node = lane
     float al, be;
     uint4 kq[KQN];                                      // chunk i: row (tid / CPR + i THREADS / CPR) mod NP
-    f32x4 s0[8][2];                                     // S0 row `col`, d_k [16s + 8hg, +8)
+    f32x4 s0[8][2];                                     // S0 row `col`, d_k 16s + 8h + 4hg + [0, 4)
     static constexpr int VQN = NP * ROW / 16 / THREADS;  // V chunks per thread
     uint4 vq[VQN];                                      // V rows, 16 bytes per chunk, coalesced
+    int cp_len, cp_node, cp_par;                        // fused commit, wave 1: path (lane l = entry l)
+    float cp_al;                                        // and alpha_prev / parent_prev of node = lane
+
+    // Order of the d_k index in the staged K/Q rows and in the S0 registers:
+    // bits 2 and 3 swapped (an involution).  With it, contraction step s of
+    // P gives lane group hg the S0 entries d_k = 16s + 4hg + [0, 4) and
+    // 16s + 8 + 4hg + [0, 4), which is the row set a 32x32 accumulator tile
+    // assigns to that lane group: an MFMA result over d_k lands directly in
+    // these registers, and each S0 load instruction reads 32 contiguous
+    // bytes of every row.
+    static __device__ __forceinline__ int kperm(int j) { return (j & ~12) | ((j & 4) << 1) | ((j & 8) >> 1); }
+
+    // Fused commit: the accepted path of unit u (lane l = entry l) with the
+    // previous round's alpha and parent of node = lane.
+    __device__ __forceinline__ void issue_path(const CommitArgs &cm, int u, int b, int lane) {
+        const int np = cm.N_prev;
+        cp_len = ld_i32(make_rsrc(cm.path_len + b, 4), 0);
+        cp_node = ld_i32(make_rsrc(cm.path + (size_t)b * cm.L_max, cm.L_max * 4), lane * 4);
+        cp_al = ld_f32(make_rsrc(cm.alpha + (size_t)u * np, np * 4), lane * 4);
+        cp_par = cm.parent ? ld_i32(make_rsrc(cm.parent + (size_t)b * np, np * 4), lane * 4) : 0;
+    }
 
     // Every HBM read of unit u, in the order the unit consumes them.
     __device__ __forceinline__ void issue(const float *S0, const In *q, const In *k, const In *vv,
@@ -100,6 +143,7 @@ struct UnitReads {
             al = ld_f32(make_rsrc(alpha + node0, N * 4), lane * 4);
             be = ld_f32(make_rsrc(beta + node0, N * 4), lane * 4);
         }
+
         const rsrc_t rk = make_rsrc(k + node0 * D, N * ROW), rq = make_rsrc(q + node0 * D, N * ROW);
 #pragma unroll
         for (int i = 0; i < KQN; ++i) {
@@ -111,24 +155,24 @@ struct UnitReads {
 #pragma unroll
         for (int i = 0; i < VQN; ++i) vq[i] = ld_u32x4<STREAM>(rv, (tid + THREADS * i) * 16);
         const rsrc_t rs = make_rsrc(S0 + (size_t)u * D * D, D * D * 4);
-        const int base = (col * D + 8 * hg) * 4;
+        const int base = (col * D + 4 * hg) * 4;
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
-            s0[s][0] = ld_f32x4<CACHED>(rs, base + 64 * s);
-            s0[s][1] = ld_f32x4<CACHED>(rs, base + 64 * s + 16);
+            s0[s][0] = ld_f32x4<CACHED>(rs, base + 64 * s);        // d_k 16s + 4hg + [0, 4)
+            s0[s][1] = ld_f32x4<CACHED>(rs, base + 64 * s + 32);   // d_k 16s + 8 + 4hg + [0, 4)
         }
     }
 };
 
-template <int NP, bool F32IN>
+template <int NP, bool F32IN, bool FUSE>
 __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_kernel(
-    const float *__restrict__ S0, const void *__restrict__ q_, const void *__restrict__ k_,
+    const float *S0, const void *__restrict__ q_, const void *__restrict__ k_,
     const void *__restrict__ v_, const float *__restrict__ alpha, const float *__restrict__ beta,
     const int32_t *__restrict__ parent, int N, int H, int units, void *__restrict__ o_,
-    float *__restrict__ U, int32_t *__restrict__ err) {
+    float *U, int32_t *__restrict__ err, CommitArgs cm) {
     using In = typename std::conditional<F32IN, float, __bf16>::type;
-    using L = VerifyLds<NP, F32IN>;
-    using Reads = UnitReads<NP, F32IN>;
+    using L = VerifyLds<NP, F32IN, FUSE>;
+    using Reads = UnitReads<NP, F32IN, FUSE>;
     constexpr int MT = NP / 32;                          // 32-row tiles of nodes
     constexpr int XS = L::XS, MS = L::MS, US = L::US, OS = L::OS;
     constexpr int CHUNK = Reads::CHUNK, CPR = Reads::CPR, KQN = Reads::KQN;
@@ -146,6 +190,14 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
     uint64_t *anc_s = reinterpret_cast<uint64_t *>(lds + L::ANC_OFF);
     int *shallow_s = reinterpret_cast<int *>(lds + L::FLAG_OFF);
     constexpr int FAST = 8;                              // ancestors a lane holds in registers
+    // fused commit staging (unused otherwise)
+    constexpr int CL = L::CL;
+    In *KpT = reinterpret_cast<In *>(lds + L::KPT_OFF);
+    float *UwT = reinterpret_cast<float *>(lds + L::UWT_OFF);
+    auto meta_node = [&](int buf) { return reinterpret_cast<int *>(lds + L::META_OFF + buf * L::META_BYTES); };
+    auto meta_w = [&](int buf) { return reinterpret_cast<float *>(lds + L::META_OFF + buf * L::META_BYTES + 256); };
+    auto meta_len = [&](int buf) { return reinterpret_cast<int *>(lds + L::META_OFF + buf * L::META_BYTES + 512); };
+    auto meta_ga = [&](int buf) { return reinterpret_cast<float *>(lds + L::META_OFF + buf * L::META_BYTES + 516); };
 
     const In *q = static_cast<const In *>(q_);
     const In *k = static_cast<const In *>(k_);
@@ -155,8 +207,51 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 
     Reads rd;
+    // Fused commit, one wave: check the previous round's accepted path of
+    // unit uu (from rd.cp_*, lane l = entry l) as treewy_commit does, and
+    // write to metadata buffer `buf` the path's nodes, the weights w_l = the
+    // product of alpha over the path entries after l (suffix products across
+    // lanes), the length, and g_a = the product over the whole path.  A bad
+    // path commits nothing.
+    auto path_meta = [&](int uu, int buf, int lane) {
+        const int bb = uu / H;
+        const bool len_ok = rd.cp_len >= 0 && rd.cp_len <= cm.L_max;
+        const int len = len_ok ? rd.cp_len : 0;
+        const int a = lane < len ? rd.cp_node : -1;
+        const int before = __shfl(a, lane > 0 ? lane - 1 : 0);
+        const int pa = lane == 0 ? -1 : before;
+        const int src = (a >= 0 && a < 64) ? a : lane;
+        const int par_a = __shfl(rd.cp_par, src);
+        const float al_a = __shfl(rd.cp_al, src);
+        bool bad = !len_ok;
+        if (lane < len) bad = bad || a < 0 || a >= cm.N_prev || a <= pa || (cm.parent && par_a != pa);
+        const bool ok = !__any(bad);
+        const int len_c = ok ? len : 0;
+        float x = lane < len_c ? al_a : 1.f;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const float y = __shfl_down(x, off);
+            x *= lane + off < 64 ? y : 1.f;
+        }
+        const float after = __shfl_down(x, 1);
+        meta_node(buf)[lane] = lane < len_c ? a : -1;
+        meta_w(buf)[lane] = lane < len_c ? (lane + 1 < 64 ? after : 1.f) : 0.f;
+        if (lane == 0) {
+            *meta_len(buf) = len_c;
+            *meta_ga(buf) = x;
+            if (!ok) flag_error(err, bb, TREEWY_FLAG_BAD_PATH);
+        }
+    };
     int u = blockIdx.x;
-    for (; u < units; u += gridDim.x) {
+    if constexpr (FUSE) {                                // path of the first unit
+        if (wave == 3 && u < units) {
+            const int lane = threadIdx.x & 63;
+            rd.issue_path(cm, u, u / H, lane);
+            path_meta(u, 0, lane);
+        }
+        __syncthreads();
+    }
+    for (int buf = 0; u < units; u += gridDim.x, buf ^= 1) {
         // Lane indices are re-derived each iteration from an opaque copy so the
         // per-lane offsets below are recomputed here instead of being hoisted
         // out of the loop and held in registers for its whole length.
@@ -165,6 +260,53 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         const int col = wave * 32 + l32;                 // this lane's d_v column (= row of S0)
         const int b = u / H;
         const size_t node0 = (size_t)u * N;              // row of node 0 of this unit in q/k/v/o/U
+
+        // Fused commit, per thread: one k chunk (KCH elements of d_k) and one
+        // U chunk (4 of d_v) of the CL path rows staged per pass.
+        constexpr int KCH = F32IN ? 4 : 8, KCPR = D / KCH;
+        const int kl = tid / KCPR, kc = (tid % KCPR) * KCH;
+        const int ul = tid / 32, uc = (tid % 32) * 4;
+        constexpr int OOB = 1 << 30;                     // past every descriptor: reads zero
+        const rsrc_t rkp = make_rsrc(FUSE ? static_cast<const In *>(cm.k) + (size_t)u * cm.N_prev * D : nullptr,
+                                     FUSE ? cm.N_prev * D * (int)sizeof(In) : 0);
+        const rsrc_t rup = make_rsrc(FUSE ? cm.U + (size_t)u * cm.N_prev * D : nullptr,
+                                     FUSE ? cm.N_prev * D * 4 : 0);
+        const int *c_node = meta_node(buf);
+        const float *c_w = meta_w(buf);
+        // Rows past the path read as zero (out-of-range offset) with weight 0.
+        auto stage_load = [&](int l0, int clen, uint4 &kv, f32x4 &uv) {
+            const int ak = (kl < CL && l0 + kl < clen) ? c_node[l0 + kl] : -1;
+            const int au = l0 + ul < clen ? c_node[l0 + ul] : -1;
+            kv = ld_u32x4<CACHED>(rkp, ak >= 0 ? (ak * D + kc) * (int)sizeof(In) : OOB);
+            uv = ld_f32x4<CACHED>(rup, au >= 0 ? (au * D + uc) * 4 : OOB);
+        };
+        auto stage_store = [&](int l0, const uint4 &kv, const f32x4 &uv) {
+            if (kl < CL) {
+                const In *kx = reinterpret_cast<const In *>(&kv);
+#pragma unroll
+                for (int e = 0; e < KCH; ++e) KpT[(kc + e) * CL + kl] = kx[e];
+            }
+            const float uw = c_w[l0 + ul];               // 0 past the path
+#pragma unroll
+            for (int e = 0; e < 4; ++e) UwT[(uc + e) * CL + ul] = uw * uv[e];
+        };
+
+        // Reads, in the order they are needed.  Fused: wave 3 first fetches
+        // the next unit's path (it turns it into metadata in phase 1), then
+        // every thread its share of this unit's first CL path rows (their
+        // nodes were found one unit ahead), then the unit's own reads.
+        int clen = 0;
+        float ga = 1.f;
+        uint4 cp_kv;
+        f32x4 cp_uv;
+        const int u_next = u + (int)gridDim.x;
+        const bool has_next = (long long)u + gridDim.x < units;
+        if constexpr (FUSE) {
+            clen = *meta_len(buf);
+            ga = *meta_ga(buf);
+            if (wave == 3 && has_next) rd.issue_path(cm, u_next, u_next / H, lane);
+            stage_load(0, clen, cp_kv, cp_uv);
+        }
         rd.issue(S0, q, k, v, alpha, beta, parent, u, b, N, tid, lane, wave, hg, col);
 
         // ---- phase 1: ancestors and cumulative decay by pointer jumping ----
@@ -200,13 +342,21 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             const bool shallow = !__any(__popcll(mask) > FAST);
             if (lane == 0) *shallow_s = shallow ? 1 : 0;
         }
-        // K and Q into LDS as bf16 (hi/lo for fp32 input), padding rows zero.
+        // Fused: the path rows (first in line) go to LDS, and wave 3, idle
+        // here, turns the next unit's path into metadata.
+        if constexpr (FUSE) {
+            stage_store(0, cp_kv, cp_uv);
+            if (wave == 3 && has_next) path_meta(u_next, buf ^ 1, lane);
+        }
+        // K and Q into LDS as bf16 (hi/lo for fp32 input), padding rows zero,
+        // with the d_k order permuted by kperm (see UnitReads::kperm).
 #pragma unroll
         for (int i = 0; i < KQN; ++i) {
             const int idx = tid + THREADS * i, r = idx / CPR, c = (idx % CPR) * CHUNK;
             const uint4 val = rd.kq[i];
             if constexpr (!F32IN) {
-                *reinterpret_cast<uint4 *>(Xh + r * XS + c) = val;
+                *reinterpret_cast<uint2 *>(Xh + r * XS + Reads::kperm(c)) = make_uint2(val.x, val.y);
+                *reinterpret_cast<uint2 *>(Xh + r * XS + Reads::kperm(c + 4)) = make_uint2(val.z, val.w);
             } else {
                 const f32x4 f = *reinterpret_cast<const f32x4 *>(&val);
                 bf16x4 hi, lo;
@@ -215,8 +365,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                     hi[e] = (__bf16)f[e];
                     lo[e] = (__bf16)(f[e] - (float)hi[e]);
                 }
-                *reinterpret_cast<bf16x4 *>(Xh + r * XS + c) = hi;
-                *reinterpret_cast<bf16x4 *>(Xl + r * XS + c) = lo;
+                *reinterpret_cast<bf16x4 *>(Xh + r * XS + Reads::kperm(c)) = hi;
+                *reinterpret_cast<bf16x4 *>(Xl + r * XS + Reads::kperm(c)) = lo;
             }
         }
         // V rows into LDS as loaded (rows of padding nodes are zero).
@@ -309,6 +459,65 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         }
 
         __syncthreads();
+        // ---- fused commit: S0 = g_a S_old + sum_l w_l U_prev[a_l] k_prev[a_l]^T
+        // The rank-L term runs on the matrix cores as (K_path^T)(w U_path)
+        // over 32-row blocks of d_k; its accumulator rows are exactly the d_k
+        // entries this lane holds of S0 (see UnitReads::kperm), so the update
+        // is elementwise.  Lane group 1 feeds zeros (CL = 8 of the 16
+        // contraction slots are used).  Paths of at most CL nodes (the usual
+        // case) update and store S0 block by block inside the P loop below,
+        // as its pieces arrive; longer paths accumulate every CL-row pass
+        // first.
+        auto rank_block = [&](int jb, f32x16 acc) {     // acc += block jb of (K_path^T)(w U_path)
+            const bf16x8 zero8 = {};
+            float uw8[8];
+            *reinterpret_cast<f32x4 *>(uw8) = *reinterpret_cast<const f32x4 *>(UwT + col * CL);
+            *reinterpret_cast<f32x4 *>(uw8 + 4) = *reinterpret_cast<const f32x4 *>(UwT + col * CL + 4);
+            bf16x8 ubh, ubl;
+            split8(uw8, ubh, ubl);
+            ubh = hg ? zero8 : ubh;
+            ubl = hg ? zero8 : ubl;
+            const In *krow = KpT + (32 * jb + l32) * CL;
+            if constexpr (F32IN) {
+                float k8[8];
+                *reinterpret_cast<f32x4 *>(k8) = *reinterpret_cast<const f32x4 *>(krow);
+                *reinterpret_cast<f32x4 *>(k8 + 4) = *reinterpret_cast<const f32x4 *>(krow + 4);
+                bf16x8 ah, alo;
+                split8(k8, ah, alo);
+                acc = mma(ah, ubh, acc);
+                acc = mma(ah, ubl, acc);
+                acc = mma(alo, ubh, acc);
+            } else {
+                const bf16x8 ah = *reinterpret_cast<const bf16x8 *>(krow);
+                acc = mma(ah, ubh, acc);
+                acc = mma(ah, ubl, acc);
+            }
+            return acc;
+        };
+        const bool upd_in_p = FUSE && clen > 0 && clen <= CL;
+        if (FUSE && clen > CL) {                        // long path: pass by pass, once S_old is in
+            for (int l0 = 0; l0 < clen; l0 += CL) {      // uniform loop
+                if (l0 > 0) {
+                    __syncthreads();
+                    uint4 kv;
+                    f32x4 uv;
+                    stage_load(l0, clen, kv, uv);
+                    stage_store(l0, kv, uv);
+                    __syncthreads();
+                }
+#pragma unroll
+                for (int jb = 0; jb < 4; ++jb) {
+                    const f32x16 d = rank_block(jb, f32x16{});
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const float x = rd.s0[2 * jb + (r >> 3)][(r >> 2) & 1][r & 3];
+                        rd.s0[2 * jb + (r >> 3)][(r >> 2) & 1][r & 3] = l0 == 0 ? fmaf(ga, x, d[r]) : x + d[r];
+                    }
+                }
+            }
+        }
+        const rsrc_t rn = make_rsrc(FUSE ? cm.S_new + (size_t)u * D * D : nullptr, FUSE ? D * D * 4 : 0);
+        const int sbase = (col * D + 4 * hg) * 4;
         const bool shallow = *shallow_s != 0;
         // ---- phase 3a: rows of T = (I + B)^{-1} for shallow trees ----------
         // (T (I + B))[t, j] = 0 for j != t gives, walking t's ancestors j from
@@ -357,7 +566,9 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 #pragma unroll
         for (int m = 0; m < 2 * MT; ++m) accp[m] = f32x16{};
         {
-            bf16x8 afr[2][2 * MT], alo[2][2 * MT];
+            // (one buffer in the fused variant, whose update block needs the registers)
+            constexpr int NBUF = FUSE ? 1 : 2;
+            bf16x8 afr[NBUF][2 * MT], alo[NBUF][2 * MT];
             auto load_a = [&](int buf, int s) {
 #pragma unroll
                 for (int m = 0; m < 2 * MT; ++m) {
@@ -366,10 +577,27 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                     if constexpr (F32IN) alo[buf][m] = *reinterpret_cast<const bf16x8 *>(arow + (Xl - Xh));
                 }
             };
-            load_a(0, 0);
+            if (NBUF == 2) load_a(0, 0);
+            f32x16 dcur = {};
 #pragma unroll
             for (int s = 0; s < 8; ++s) {
-                if (s < 7) load_a((s + 1) & 1, s + 1);
+                if (NBUF == 1)
+                    load_a(0, s);
+                else if (s < 7)
+                    load_a((s + 1) & 1, s + 1);
+                if constexpr (FUSE) {                    // S0 pieces of step s: commit update, then S_new
+                    if (upd_in_p) {
+                        if ((s & 1) == 0) dcur = rank_block(s >> 1, f32x16{});
+#pragma unroll
+                        for (int h = 0; h < 2; ++h)
+#pragma unroll
+                            for (int i = 0; i < 4; ++i)
+                                rd.s0[s][h][i] = fmaf(ga, rd.s0[s][h][i], dcur[8 * (s & 1) + 4 * h + i]);
+                    }
+#pragma unroll
+                    for (int h = 0; h < 2; ++h)
+                        st_u32x4<CACHED>(rn, sbase + 64 * s + 32 * h, __builtin_bit_cast(uint4, rd.s0[s][h]));
+                }
                 float sv[8];
                 *reinterpret_cast<f32x4 *>(sv) = rd.s0[s][0];
                 *reinterpret_cast<f32x4 *>(sv + 4) = rd.s0[s][1];
@@ -377,9 +605,9 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 split8(sv, bh, bl);
 #pragma unroll
                 for (int m = 0; m < 2 * MT; ++m) {
-                    accp[m] = mma(afr[s & 1][m], bh, accp[m]);
-                    accp[m] = mma(afr[s & 1][m], bl, accp[m]);
-                    if constexpr (F32IN) accp[m] = mma(alo[s & 1][m], bh, accp[m]);
+                    accp[m] = mma(afr[s % NBUF][m], bh, accp[m]);
+                    accp[m] = mma(afr[s % NBUF][m], bl, accp[m]);
+                    if constexpr (F32IN) accp[m] = mma(alo[s % NBUF][m], bh, accp[m]);
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -516,7 +744,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 
 namespace {
 
-template <int NP, bool F32IN>
+template <int NP, bool F32IN, bool FUSE>
 int resident_grid(int units) {
     static int per_device[64] = {0};
     int dev = 0;
@@ -525,7 +753,7 @@ int resident_grid(int units) {
         int cus = 0, blocks = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
             cus = 256;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, verify_kernel<NP, F32IN>, THREADS, 0) !=
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, verify_kernel<NP, F32IN, FUSE>, THREADS, 0) !=
                 hipSuccess || blocks <= 0)
             blocks = 1;
         per_device[dev] = cus * blocks;
@@ -533,14 +761,25 @@ int resident_grid(int units) {
     return units < per_device[dev] ? units : per_device[dev];
 }
 
-template <int NP, bool F32IN>
+template <int NP, bool F32IN, bool FUSE>
 hipError_t launch(const float *S0, const void *q, const void *k, const void *v, const float *alpha,
                   const float *beta, const int32_t *parent, int N, int B, int H, void *o, float *U,
-                  int32_t *err, hipStream_t stream) {
+                  int32_t *err, const CommitArgs &cm, hipStream_t stream) {
     const int units = B * H;
-    hipLaunchKernelGGL((verify_kernel<NP, F32IN>), dim3((unsigned)resident_grid<NP, F32IN>(units)),
-                       dim3(THREADS), 0, stream, S0, q, k, v, alpha, beta, parent, N, H, units, o, U, err);
+    hipLaunchKernelGGL((verify_kernel<NP, F32IN, FUSE>), dim3((unsigned)resident_grid<NP, F32IN, FUSE>(units)),
+                       dim3(THREADS), 0, stream, S0, q, k, v, alpha, beta, parent, N, H, units, o, U, err, cm);
     return hipGetLastError();
+}
+
+template <bool FUSE>
+hipError_t dispatch(const float *S0, const void *q, const void *k, const void *v, const float *alpha,
+                    const float *beta, const int32_t *parent, int N, int B, int H, bool f32_in, void *o,
+                    float *U, int32_t *err, const CommitArgs &cm, hipStream_t stream) {
+    if (N <= 32)
+        return f32_in ? launch<32, true, FUSE>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream)
+                      : launch<32, false, FUSE>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream);
+    return f32_in ? launch<64, true, FUSE>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream)
+                  : launch<64, false, FUSE>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream);
 }
 
 }  // namespace
@@ -549,11 +788,18 @@ hipError_t launch_verify(const float *S0, const void *q, const void *k, const vo
                          const float *alpha, const float *beta, const int32_t *parent, int N,
                          int B, int H, bool f32_in, void *o, float *U, int32_t *err,
                          hipStream_t stream) {
-    if (N <= 32)
-        return f32_in ? launch<32, true>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, stream)
-                      : launch<32, false>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, stream);
-    return f32_in ? launch<64, true>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, stream)
-                  : launch<64, false>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, stream);
+    const CommitArgs none = {};
+    return dispatch<false>(S0, q, k, v, alpha, beta, parent, N, B, H, f32_in, o, U, err, none, stream);
+}
+
+hipError_t launch_commit_verify(const float *S_old, const float *U_prev, const void *k_prev,
+                                const float *alpha_prev, const int32_t *path, const int32_t *path_len,
+                                int L_max, const int32_t *parent_prev, int N_prev, const void *q,
+                                const void *k, const void *v, const float *alpha, const float *beta,
+                                const int32_t *parent, int N, int B, int H, bool f32_in, float *S_new,
+                                void *o, float *U, int32_t *err, hipStream_t stream) {
+    const CommitArgs cm = {U_prev, k_prev, alpha_prev, path, path_len, parent_prev, S_new, L_max, N_prev};
+    return dispatch<true>(S_old, q, k, v, alpha, beta, parent, N, B, H, f32_in, o, U, err, cm, stream);
 }
 
 }  // namespace treewy

@@ -9,6 +9,8 @@ library has not been built, importing this module raises.
 Function names match the C ABI:
   treewy_verify(S0, q, k, v, alpha, beta, parent) -> (o, U)
   treewy_commit(S0, U, k, alpha, path, path_len, parent=None) -> S_new
+  treewy_commit_verify(S_old, U_prev, k_prev, alpha_prev, path, path_len,
+                       q, k, v, alpha, beta, parent, parent_prev=None) -> (S_new, o, U)
   treewy_snapshot_verify(S0, q, k, v, alpha, beta, parent) -> (o, snapshots)
   treewy_snapshot_commit(S0, snapshots, accepted) -> S_new
   treewy_path_from_node(parent, accepted, L_max) -> (path, path_len)
@@ -39,6 +41,8 @@ lib.treewy_verify.argtypes = [_P] * 7 + [_I] * 6 + [_P] * 4
 lib.treewy_verify.restype = _I
 lib.treewy_commit.argtypes = [_P] * 6 + [_I, _P] + [_I] * 6 + [_P] * 3
 lib.treewy_commit.restype = _I
+lib.treewy_commit_verify.argtypes = [_P] * 6 + [_I, _P, _I] + [_P] * 6 + [_I] * 6 + [_P] * 5
+lib.treewy_commit_verify.restype = _I
 lib.treewy_snapshot_verify.argtypes = [_P] * 7 + [_I] * 6 + [_P] * 4
 lib.treewy_snapshot_verify.restype = _I
 lib.treewy_snapshot_commit.argtypes = [_P] * 3 + [_I] * 5 + [_P] * 3
@@ -48,8 +52,8 @@ lib.treewy_path_from_node.restype = _I
 lib.treewy_status_string.argtypes = [_I]
 lib.treewy_status_string.restype = ctypes.c_char_p
 
-EXPORTED = ("treewy_verify", "treewy_commit", "treewy_snapshot_verify", "treewy_snapshot_commit",
-            "treewy_path_from_node", "treewy_status_string")
+EXPORTED = ("treewy_verify", "treewy_commit", "treewy_commit_verify", "treewy_snapshot_verify",
+            "treewy_snapshot_commit", "treewy_path_from_node", "treewy_status_string")
 
 
 class TreewyError(RuntimeError):
@@ -134,6 +138,41 @@ def treewy_commit(S0, U, k, alpha, path, path_len, parent=None, S_new=None, err=
                              _ptr(parent), N, B, H, dk, dv, _in_dtype(k), _ptr(S_new), _ptr(err),
                              _stream(stream)), "treewy_commit")
     return S_new
+
+
+def treewy_commit_verify(S_old, U_prev, k_prev, alpha_prev, path, path_len, q, k, v, alpha, beta, parent,
+                         parent_prev=None, S_new=None, o=None, U=None, err=None, stream=None
+                         ) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    B, H, N, dk = q.shape
+    dv = v.shape[-1]
+    N_prev = k_prev.shape[2]
+    L_max = path.shape[1]
+    dt = q.dtype
+    _need(S_old, "S_old", torch.float32, (B, H, dv, dk))
+    _need(U_prev, "U_prev", torch.float32, (B, H, N_prev, dv)); _need(k_prev, "k_prev", dt, (B, H, N_prev, dk))
+    _need(alpha_prev, "alpha_prev", torch.float32, (B, H, N_prev))
+    _need(path, "path", torch.int32, (B, L_max)); _need(path_len, "path_len", torch.int32, (B,))
+    if parent_prev is not None:
+        _need(parent_prev, "parent_prev", torch.int32, (B, N_prev))
+    _need(q, "q", dt, (B, H, N, dk)); _need(k, "k", dt, (B, H, N, dk)); _need(v, "v", dt, (B, H, N, dv))
+    _need(alpha, "alpha", torch.float32, (B, H, N)); _need(beta, "beta", torch.float32, (B, H, N))
+    _need(parent, "parent", torch.int32, (B, N))
+    if S_new is None:
+        S_new = torch.empty_like(S_old)
+    if o is None:
+        o = torch.empty((B, H, N, dv), dtype=dt, device=q.device)
+    if U is None:
+        U = torch.empty((B, H, N, dv), dtype=torch.float32, device=q.device)
+    _need(S_new, "S_new", torch.float32, (B, H, dv, dk))
+    _need(o, "o", dt, (B, H, N, dv)); _need(U, "U", torch.float32, (B, H, N, dv))
+    if err is not None:
+        _need(err, "err", torch.int32, (B,))
+    _check(lib.treewy_commit_verify(_ptr(S_old), _ptr(U_prev), _ptr(k_prev), _ptr(alpha_prev), _ptr(path),
+                                    _ptr(path_len), L_max, _ptr(parent_prev), N_prev, _ptr(q), _ptr(k), _ptr(v),
+                                    _ptr(alpha), _ptr(beta), _ptr(parent), N, B, H, dk, dv, _in_dtype(q),
+                                    _ptr(S_new), _ptr(o), _ptr(U), _ptr(err), _stream(stream)),
+           "treewy_commit_verify")
+    return S_new, o, U
 
 
 def treewy_snapshot_verify(S0, q, k, v, alpha, beta, parent, o=None, snapshots=None, err=None,

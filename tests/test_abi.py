@@ -24,7 +24,7 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    assert names == sorted(["treewy_verify", "treewy_commit", "treewy_snapshot_verify",
+    assert names == sorted(["treewy_verify", "treewy_commit", "treewy_commit_verify", "treewy_snapshot_verify",
                             "treewy_snapshot_commit", "treewy_path_from_node", "treewy_status_string"])
 
 
@@ -79,6 +79,35 @@ def test_commit_host_checks(tw):
     assert call(S_new=M) == tw.TREEWY_ERR_INVALID_ARG
     assert call(dt=2) == tw.TREEWY_ERR_INVALID_ARG
     assert call(B=0, S0=None) == tw.TREEWY_OK
+
+
+def test_commit_verify_host_checks(tw):
+    f = tw.lib.treewy_commit_verify
+
+    def call(S_old=A, U_prev=A, k_prev=A, path=A, plen=A, L_max=8, N_prev=8, q=A, N=8, B=2, H=2, dk=128,
+             dt=1, S_new=A, o=A, U=A):
+        return f(S_old, U_prev, k_prev, A, path, plen, L_max, None, N_prev, q, A, A, A, A, A, N, B, H, dk, 128,
+                 dt, S_new, o, U, None, None)
+
+    assert call(dk=64) == tw.TREEWY_ERR_UNSUPPORTED
+    assert call(N=65) == tw.TREEWY_ERR_UNSUPPORTED
+    assert call(N_prev=65) == tw.TREEWY_ERR_UNSUPPORTED
+    assert call(L_max=65) == tw.TREEWY_ERR_UNSUPPORTED
+    assert call(N_prev=-1) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(L_max=-1) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(dt=3) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(S_old=None) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(plen=None) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(path=None) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(U_prev=None) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(q=None) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(o=None) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(S_new=M) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(k_prev=M) == tw.TREEWY_ERR_INVALID_ARG
+    # U over U_prev is allowed only when both rounds have the same N
+    assert call(U_prev=A, U=A, N_prev=4) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(B=0, S_old=None) == tw.TREEWY_OK
+    assert call(H=0, S_old=None) == tw.TREEWY_OK
 
 
 def test_snapshot_commit_and_path_host_checks(tw):
