@@ -303,6 +303,21 @@ def main():
         kernel="treewy_commit_verify", nodes_per_s=round(nodes / (ms_fused * 1e-3), 1),
         speedup_vs_separate_calls=round(ms_step / ms_fused, 3))
     del S_fused, o_f, U_f
+    # Greedy acceptance on the device (tokens: vocabulary of 4, the target
+    # agreeing with the drafter along one planted chain per sequence).
+    tok = wl.acceptance_tokens(x["parent"], seed=args.seed, vocab=4, plant=True)
+    t_d, t_t, t_r = (torch.from_numpy(tok[n]).to("cuda") for n in ("draft", "target", "root"))
+    acc_path = torch.empty((w.B, w.max_depth), dtype=torch.int32, device="cuda")
+    acc_len = torch.empty((w.B,), dtype=torch.int32, device="cuda")
+    acc_bonus = torch.empty((w.B,), dtype=torch.int32, device="cuda")
+
+    def accept():
+        tw.treewy_accept_greedy(d["parent"], t_d, t_t, t_r, w.max_depth, path=acc_path, path_len=acc_len,
+                                bonus=acc_bonus)
+
+    _, (ms_acc,) = time_steps(torch, [accept], args.steps, args.warmup)
+    result["accept_greedy"] = {"avg_launch_ms": round(ms_acc, 5), "sequences": w.B, "nodes": w.N,
+                               "mean_accepted": round(float(acc_len.float().mean()), 3)}
     spec = acc.speculative_state_bytes(w)
     result["speculative_state_bytes"] = {"treewy_U": spec["treewy_U"], "treewy_U_k_alpha": spec["treewy_U_k_alpha"],
                                          "snapshot_states": spec["snapshot_states"]}

@@ -174,6 +174,32 @@ treewy_status treewy_path_from_node(const int32_t *parent, const int32_t *accept
                                     int L_max, int32_t *path, int32_t *path_len, int32_t *err,
                                     void *stream);
 
+/*
+ * treewy_accept_greedy - greedy acceptance of the draft tree, on the device
+ * (Background: the target keeps the longest run of draft tokens it would have
+ * generated itself; the paper verifies greedily, Implementation).  From the
+ * committed prefix, move to the child whose draft token equals the target's
+ * prediction at the current position (the lowest index among equal siblings)
+ * until no child matches.  The accepted path comes out in the layout
+ * treewy_commit and treewy_commit_verify read, with no host round trip.
+ * Bit exact.
+ *   parent       [B, N] int32
+ *   draft_token  [B, N] int32              token proposed at node t
+ *   target_token [B, N] int32              the target's greedy next token after node t
+ *   root_token   [B] int32                 the target's greedy next token after the committed prefix
+ *   path         [B, L_max] int32 written  accepted nodes, root first, then -1
+ *   path_len     [B] int32 written
+ *   bonus        [B] int32 or NULL         written: the target's token after the last accepted node
+ *                                          (root_token when nothing is accepted)
+ *   err          [B] int32 or NULL         BAD_PARENT (that parent counts as -1); BAD_PATH when the
+ *                                          accepted path is longer than L_max (then path_len = 0;
+ *                                          bonus is still the end of the full walk)
+ */
+treewy_status treewy_accept_greedy(const int32_t *parent, const int32_t *draft_token,
+                                   const int32_t *target_token, const int32_t *root_token, int N, int B,
+                                   int L_max, int32_t *path, int32_t *path_len, int32_t *bonus,
+                                   int32_t *err, void *stream);
+
 /* Static description of a status code; never NULL. */
 const char *treewy_status_string(treewy_status status);
 

@@ -129,6 +129,21 @@ treewy_status treewy_path_from_node(const int32_t *parent, const int32_t *accept
                                                     err, static_cast<hipStream_t>(stream)));
 }
 
+treewy_status treewy_accept_greedy(const int32_t *parent, const int32_t *draft_token,
+                                   const int32_t *target_token, const int32_t *root_token, int N, int B,
+                                   int L_max, int32_t *path, int32_t *path_len, int32_t *bonus,
+                                   int32_t *err, void *stream) {
+    if (N < 0 || B < 0 || L_max < 0) return TREEWY_ERR_INVALID_ARG;
+    if (N > kMaxN || L_max > kMaxN) return TREEWY_ERR_UNSUPPORTED;
+    if (B == 0) return TREEWY_OK;
+    if (!root_token || !path_len || (N > 0 && (!parent || !draft_token || !target_token)) ||
+        (L_max > 0 && !path))
+        return TREEWY_ERR_INVALID_ARG;
+    return hip_status(treewy::launch_accept_greedy(parent, draft_token, target_token, root_token, N, B, L_max,
+                                                   path, path_len, bonus, err,
+                                                   static_cast<hipStream_t>(stream)));
+}
+
 const char *treewy_status_string(treewy_status status) {
     switch (status) {
     case TREEWY_OK: return "ok";

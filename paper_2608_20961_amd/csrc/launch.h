@@ -38,4 +38,8 @@ hipError_t launch_path_from_node(const int32_t *parent, const int32_t *accepted,
                                  int L_max, int32_t *path, int32_t *path_len, int32_t *err,
                                  hipStream_t stream);
 
+hipError_t launch_accept_greedy(const int32_t *parent, const int32_t *draft, const int32_t *target,
+                                const int32_t *root, int N, int B, int L_max, int32_t *path,
+                                int32_t *path_len, int32_t *bonus, int32_t *err, hipStream_t stream);
+
 }  // namespace treewy

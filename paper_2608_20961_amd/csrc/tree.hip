@@ -1,6 +1,9 @@
-// treewy_path_from_node kernel: root-to-node path of each sequence's accepted
-// node (the accepted node's ancestors and itself, Method eq. 3), one thread
-// per sequence.  Integer work only, so the result is exact.
+// Tree helpers, integer work only (results are exact):
+//  - treewy_path_from_node: root-to-node path of each sequence's accepted node
+//    (the accepted node's ancestors and itself, Method eq. 3), one thread per
+//    sequence;
+//  - treewy_accept_greedy: greedy acceptance of the draft tree, one wave per
+//    sequence with lane t holding node t.
 #include "device.h"
 #include "launch.h"
 
@@ -37,6 +40,60 @@ __global__ __launch_bounds__(THREADS) void path_from_node_kernel(
     }
     for (int l = len; l < L_max; ++l) out[l] = -1;
     path_len[b] = len;
+}
+
+// Greedy acceptance (Background: the target keeps the longest run of draft
+// tokens it would have generated itself; the paper verifies greedily,
+// Implementation).  From the committed prefix, repeatedly move to the child
+// whose draft token equals the target's prediction at the current position
+// (lowest index among equal siblings) until no child matches.  Children have
+// larger indices than their parent, so the walk ends within N steps.
+__global__ __launch_bounds__(THREADS) void accept_greedy_kernel(
+    const int32_t *__restrict__ parent, const int32_t *__restrict__ draft,
+    const int32_t *__restrict__ target, const int32_t *__restrict__ root, int N, int B, int L_max,
+    int32_t *__restrict__ path, int32_t *__restrict__ path_len, int32_t *__restrict__ bonus,
+    int32_t *__restrict__ err) {
+    const int lane = threadIdx.x & 63;
+    const int b = blockIdx.x * (THREADS / 64) + (threadIdx.x >> 6);
+    if (b >= B) return;                                  // whole waves leave together
+    const size_t row = (size_t)b * N;
+    int par = -1, tok = 0, pred = 0;
+    if (lane < N) {
+        par = parent[row + lane];
+        tok = draft[row + lane];
+        pred = target[row + lane];
+        if (par < -1 || par >= lane) {
+            flag_error(err, b, TREEWY_FLAG_BAD_PARENT);
+            par = -1;
+        }
+    }
+    int pos = -1, want = root[b], len = 0, mine = -1;    // lane l keeps the l-th accepted node
+    while (true) {
+        const uint64_t m = __ballot(lane < N && par == pos && tok == want);
+        if (m == 0) break;
+        const int c = __builtin_ctzll(m);
+        if (lane == len) mine = c;
+        ++len;
+        want = __shfl(pred, c);
+        pos = c;
+    }
+    const bool fits = len <= L_max;
+    if (!fits && lane == 0) flag_error(err, b, TREEWY_FLAG_BAD_PATH);
+    if (lane < L_max) path[(size_t)b * L_max + lane] = fits && lane < len ? mine : -1;
+    if (lane == 0) {
+        path_len[b] = fits ? len : 0;
+        if (bonus) bonus[b] = want;
+    }
+}
+
+hipError_t launch_accept_greedy(const int32_t *parent, const int32_t *draft, const int32_t *target,
+                                const int32_t *root, int N, int B, int L_max, int32_t *path,
+                                int32_t *path_len, int32_t *bonus, int32_t *err, hipStream_t stream) {
+    const int per_block = THREADS / 64;
+    const int blocks = (B + per_block - 1) / per_block;
+    hipLaunchKernelGGL(accept_greedy_kernel, dim3((unsigned)blocks), dim3(THREADS), 0, stream, parent,
+                       draft, target, root, N, B, L_max, path, path_len, bonus, err);
+    return hipGetLastError();
 }
 
 hipError_t launch_path_from_node(const int32_t *parent, const int32_t *accepted, int N, int B,

@@ -14,6 +14,7 @@ Function names match the C ABI:
   treewy_snapshot_verify(S0, q, k, v, alpha, beta, parent) -> (o, snapshots)
   treewy_snapshot_commit(S0, snapshots, accepted) -> S_new
   treewy_path_from_node(parent, accepted, L_max) -> (path, path_len)
+  treewy_accept_greedy(parent, draft_token, target_token, root_token, L_max) -> (path, path_len, bonus)
 """
 from __future__ import annotations
 
@@ -49,11 +50,13 @@ lib.treewy_snapshot_commit.argtypes = [_P] * 3 + [_I] * 5 + [_P] * 3
 lib.treewy_snapshot_commit.restype = _I
 lib.treewy_path_from_node.argtypes = [_P, _P, _I, _I, _I, _P, _P, _P, _P]
 lib.treewy_path_from_node.restype = _I
+lib.treewy_accept_greedy.argtypes = [_P] * 4 + [_I] * 3 + [_P] * 5
+lib.treewy_accept_greedy.restype = _I
 lib.treewy_status_string.argtypes = [_I]
 lib.treewy_status_string.restype = ctypes.c_char_p
 
 EXPORTED = ("treewy_verify", "treewy_commit", "treewy_commit_verify", "treewy_snapshot_verify",
-            "treewy_snapshot_commit", "treewy_path_from_node", "treewy_status_string")
+            "treewy_snapshot_commit", "treewy_path_from_node", "treewy_accept_greedy", "treewy_status_string")
 
 
 class TreewyError(RuntimeError):
@@ -227,3 +230,27 @@ def treewy_path_from_node(parent, accepted, L_max, path=None, path_len=None, err
     _check(lib.treewy_path_from_node(_ptr(parent), _ptr(accepted), N, B, L_max, _ptr(path), _ptr(path_len),
                                      _ptr(err), _stream(stream)), "treewy_path_from_node")
     return path, path_len
+
+
+def treewy_accept_greedy(parent, draft_token, target_token, root_token, L_max: int, path=None, path_len=None,
+                         bonus=None, err=None, stream=None) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    B, N = parent.shape
+    _need(parent, "parent", torch.int32, (B, N))
+    _need(draft_token, "draft_token", torch.int32, (B, N))
+    _need(target_token, "target_token", torch.int32, (B, N))
+    _need(root_token, "root_token", torch.int32, (B,))
+    dev = parent.device
+    if path is None:
+        path = torch.empty((B, L_max), dtype=torch.int32, device=dev)
+    if path_len is None:
+        path_len = torch.empty((B,), dtype=torch.int32, device=dev)
+    if bonus is None:
+        bonus = torch.empty((B,), dtype=torch.int32, device=dev)
+    _need(path, "path", torch.int32, (B, L_max)); _need(path_len, "path_len", torch.int32, (B,))
+    _need(bonus, "bonus", torch.int32, (B,))
+    if err is not None:
+        _need(err, "err", torch.int32, (B,))
+    _check(lib.treewy_accept_greedy(_ptr(parent), _ptr(draft_token), _ptr(target_token), _ptr(root_token), N, B,
+                                    L_max, _ptr(path), _ptr(path_len), _ptr(bonus), _ptr(err), _stream(stream)),
+           "treewy_accept_greedy")
+    return path, path_len, bonus

@@ -302,6 +302,31 @@ def warmup_tokens(w: Workload, seed: int = 0, units: Optional[slice] = None,
     return {n: np.stack(a) if a else np.zeros((0,)) for n, a in out.items()}
 
 
+def acceptance_tokens(parents: np.ndarray, seed: int = 0, vocab: int = 4, plant: bool = True
+                      ) -> Dict[str, np.ndarray]:
+    """Synthetic tokens for greedy acceptance over the trees `parents` [B, N].
+
+    draft [B, N]: the token proposed at each node; target [B, N]: the target's
+    next token after each node; root [B]: its next token after the committed
+    prefix, all uniform in [0, vocab).  With `plant`, the target agrees with
+    the drafter along one random root-to-node chain per sequence, so long
+    acceptances occur.
+    """
+    parents = np.asarray(parents)
+    B, N = parents.shape
+    rng = np.random.default_rng(np.random.SeedSequence([20961, 7, int(seed), B, N, int(vocab)]))
+    draft = rng.integers(0, vocab, (B, N)).astype(np.int32)
+    target = rng.integers(0, vocab, (B, N)).astype(np.int32)
+    root = rng.integers(0, vocab, B).astype(np.int32)
+    if plant and N > 0:
+        for b in range(B):
+            chain = ancestors_and_self(parents[b], int(rng.integers(N)))
+            root[b] = draft[b, chain[0]]
+            for a, c in zip(chain[:-1], chain[1:]):
+                target[b, a] = draft[b, c]
+    return dict(draft=draft, target=target, root=root)
+
+
 def sample_units(w: Workload, count: int, seed: int = 0) -> np.ndarray:
     """A reproducible sample of unit ids (b * H + h), always including the first and last."""
     rng = np.random.default_rng(np.random.SeedSequence([20961, 5, int(seed), w.units]))

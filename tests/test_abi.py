@@ -25,7 +25,8 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     assert names == sorted(["treewy_verify", "treewy_commit", "treewy_commit_verify", "treewy_snapshot_verify",
-                            "treewy_snapshot_commit", "treewy_path_from_node", "treewy_status_string"])
+                            "treewy_snapshot_commit", "treewy_path_from_node", "treewy_accept_greedy",
+                            "treewy_status_string"])
 
 
 def test_library_exports_every_declared_symbol(tw):
@@ -116,6 +117,23 @@ def test_snapshot_commit_and_path_host_checks(tw):
     assert tw.lib.treewy_path_from_node(A, A, 65, 2, 8, A, A, None, None) == tw.TREEWY_ERR_UNSUPPORTED
     assert tw.lib.treewy_path_from_node(A, None, 8, 2, 8, A, A, None, None) == tw.TREEWY_ERR_INVALID_ARG
     assert tw.lib.treewy_path_from_node(None, None, 8, 0, 8, None, None, None, None) == tw.TREEWY_OK
+
+
+def test_accept_greedy_host_checks(tw):
+    f = tw.lib.treewy_accept_greedy
+
+    def call(parent=A, draft=A, target=A, root=A, N=8, B=2, L_max=8, path=A, plen=A):
+        return f(parent, draft, target, root, N, B, L_max, path, plen, None, None, None)
+
+    assert call(N=65) == tw.TREEWY_ERR_UNSUPPORTED
+    assert call(L_max=65) == tw.TREEWY_ERR_UNSUPPORTED
+    assert call(N=-1) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(B=-1) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(root=None) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(draft=None) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(plen=None) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(path=None) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(B=0, root=None, plen=None) == tw.TREEWY_OK
 
 
 def test_binding_raises_with_status(tw):
