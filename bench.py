@@ -303,6 +303,40 @@ def main():
         kernel="treewy_commit_verify", nodes_per_s=round(nodes / (ms_fused * 1e-3), 1),
         speedup_vs_separate_calls=round(ms_step / ms_fused, 3))
     del S_fused, o_f, U_f
+    # bf16 state storage: the same step with S0 / S_new in bfloat16 (inputs
+    # rounded once from the float32 state).
+    if w.in_dtype == "bf16":
+        S0_b = d["S0"].to(torch.bfloat16)
+        S0_bc = S0_b.clone()
+        S_new_b = torch.empty_like(S0_b)
+        o_b, U_b = torch.empty_like(o), torch.empty_like(U)
+
+        def verify_b():
+            tw.treewy_verify(S0_b, d["q"], d["k"], d["v"], d["alpha"], d["beta"], d["parent"], o=o_b, U=U_b)
+
+        def commit_b():
+            tw.treewy_commit(S0_bc, U_b, d["k"], d["alpha"], d["path"], d["path_len"], parent=d["parent"],
+                             S_new=S_new_b)
+
+        def fused_b():
+            tw.treewy_commit_verify(S0_bc, U_b, d["k"], d["alpha"], d["path"], d["path_len"], d["q"], d["k"],
+                                    d["v"], d["alpha"], d["beta"], d["parent"], parent_prev=d["parent"],
+                                    S_new=S_new_b, o=o_f2, U=U_f2)
+
+        o_f2, U_f2 = torch.empty_like(o), torch.empty_like(U)
+        ms_step_b, (ms_vb, ms_cb) = time_steps(torch, [verify_b, commit_b], args.steps, args.warmup)
+        _, (ms_fb,) = time_steps(torch, [fused_b], args.steps, args.warmup)
+        log("bf16 state: verify %.4f, commit %.4f, fused %.4f ms" % (ms_vb, ms_cb, ms_fb))
+        result["bf16_state"] = {
+            "ms_per_step": round(ms_step_b, 5), "nodes_per_s": round(nodes / (ms_step_b * 1e-3), 1),
+            "verify": roofline(acc.verify_bytes(w, 2), ms_vb, load_traffic("verify_bf16state", w.name, src_hash)),
+            "commit": roofline(acc.commit_bytes(w, x["path_len"], 2), ms_cb,
+                               load_traffic("commit_bf16state", w.name, src_hash)),
+            "fused_commit_verify": roofline(acc.commit_verify_bytes(w, x["path_len"], 2), ms_fb,
+                                            load_traffic("commit_verify_bf16state", w.name, src_hash)),
+            "speedup_vs_f32_state": round(ms_step / ms_step_b, 3),
+        }
+        del S0_b, S0_bc, S_new_b, o_b, U_b, o_f2, U_f2
     # Greedy acceptance on the device (tokens: vocabulary of 4, the target
     # agreeing with the drafter along one planted chain per sequence).
     tok = wl.acceptance_tokens(x["parent"], seed=args.seed, vocab=4, plant=True)

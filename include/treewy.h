@@ -50,9 +50,15 @@ typedef enum treewy_status {
 } treewy_status;
 
 typedef enum treewy_dtype {
-    TREEWY_F32 = 0,              /* q, k, v and o in float32 */
-    TREEWY_BF16 = 1              /* q, k, v and o in bfloat16 (state, U, alpha, beta stay float32) */
+    TREEWY_F32 = 0,              /* float32 */
+    TREEWY_BF16 = 1              /* bfloat16 */
 } treewy_dtype;
+/* in_dtype / k_dtype name the type of q, k, v and o.  state_dtype names the
+ * type of S0 / S_new: float32, or bfloat16 (the state storage the paper's
+ * vLLM accounting assumes, Section "The memory problem") with bfloat16 inputs
+ * only.  A bfloat16 state is read exactly, all arithmetic stays float32, and
+ * S_new is rounded to nearest even once when written.  U, alpha and beta are
+ * always float32. */
 
 #define TREEWY_FLAG_BAD_PARENT 1 /* some parent[b][t] outside [-1, t-1]; treated as -1 */
 #define TREEWY_FLAG_BAD_PATH 2   /* path[b] is not a root-to-node path; state left unchanged */
@@ -68,7 +74,7 @@ typedef enum treewy_dtype {
  *   o_t = g_t S0 q_t + sum over i ancestor-or-self of t of (g_t/g_i) (k_i . q_t) U[i]
  * out of the same solve (equal to S_t q_t of eq. 1).
  *
- *   S0     [B, H, d_v, d_k] float32        committed states (read only)
+ *   S0     [B, H, d_v, d_k] state_dtype    committed states (read only)
  *   q, k   [B, H, N, d_k]   in_dtype
  *   v      [B, H, N, d_v]   in_dtype
  *   alpha, beta [B, H, N]   float32
@@ -77,9 +83,9 @@ typedef enum treewy_dtype {
  *   U      [B, H, N, d_v]   float32        written: pseudo-values, read by treewy_commit
  *   err    [B] int32 or NULL               TREEWY_FLAG_BAD_PARENT
  */
-treewy_status treewy_verify(const float *S0, const void *q, const void *k, const void *v,
+treewy_status treewy_verify(const void *S0, const void *q, const void *k, const void *v,
                             const float *alpha, const float *beta, const int32_t *parent, int N,
-                            int B, int H, int d_k, int d_v, treewy_dtype in_dtype,
+                            int B, int H, int d_k, int d_v, treewy_dtype in_dtype, treewy_dtype state_dtype,
                             void *o, float *U, int32_t *err, void *stream);
 
 /*
@@ -87,21 +93,22 @@ treewy_status treewy_verify(const float *S0, const void *q, const void *k, const
  *   S_a = g_a S0 + sum over i on the root-to-a path of (g_a/g_i) U[i] k_i^T,
  * which becomes the next round's S0.  Replaces full-state snapshotting.
  *
- *   S0       [B, H, d_v, d_k] float32      committed states
+ *   S0       [B, H, d_v, d_k] state_dtype  committed states
  *   U        [B, H, N, d_v]   float32      pseudo-values from treewy_verify
  *   k        [B, H, N, d_k]   k_dtype      the keys given to treewy_verify
  *   alpha    [B, H, N]        float32
  *   path     [B, L_max]       int32        root -> accepted node; entries past path_len ignored
  *   path_len [B]              int32        0 = nothing accepted: S_new = S0 bit for bit
  *   parent   [B, N] int32 or NULL          when given, each path is checked against the tree
- *   S_new    [B, H, d_v, d_k] float32      written; may be the same buffer as S0 (in place)
+ *   S_new    [B, H, d_v, d_k] state_dtype  written; may be the same buffer as S0 (in place)
  *   err      [B] int32 or NULL             TREEWY_FLAG_BAD_PATH (that sequence keeps S0)
  * Without `parent` a path is only checked to be strictly increasing and in [0, N).
  */
-treewy_status treewy_commit(const float *S0, const float *U, const void *k, const float *alpha,
+treewy_status treewy_commit(const void *S0, const float *U, const void *k, const float *alpha,
                             const int32_t *path, const int32_t *path_len, int L_max,
                             const int32_t *parent, int N, int B, int H, int d_k, int d_v,
-                            treewy_dtype k_dtype, float *S_new, int32_t *err, void *stream);
+                            treewy_dtype k_dtype, treewy_dtype state_dtype, void *S_new, int32_t *err,
+                            void *stream);
 
 /*
  * treewy_commit_verify - the previous round's commit fused into this round's
@@ -114,33 +121,36 @@ treewy_status treewy_commit(const float *S0, const float *U, const void *k, cons
  * but reads the state once: S_new is formed in registers, written, and used
  * as this round's S0 without a second read.
  *
- *   S_old      [B, H, d_v, d_k] float32    committed state before the previous round
+ *   S_old      [B, H, d_v, d_k] state_dtype committed state before the previous round
  *   U_prev     [B, H, N_prev, d_v] float32 the previous round's pseudo-values
  *   k_prev     [B, H, N_prev, d_k] in_dtype its keys
  *   alpha_prev [B, H, N_prev] float32      its decay gates
  *   path, path_len, L_max                  its accepted paths, as for treewy_commit
  *   parent_prev [B, N_prev] int32 or NULL  its tree, to check the paths
  *   q, k, v, alpha, beta, parent, N        this round's draft, as for treewy_verify
- *   S_new      [B, H, d_v, d_k] float32    written; may be the same buffer as S_old
+ *   S_new      [B, H, d_v, d_k] state_dtype written (a bf16 state: rounded, and this round verifies
+ *                                          from the rounded value, as the separate calls do);
+ *                                          may be the same buffer as S_old
  *   o, U                                    written, as for treewy_verify
  *   err        [B] int32 or NULL           BAD_PATH (that sequence's S_new = S_old) | BAD_PARENT
  * 0 <= N_prev <= 64.  U may be the same buffer as U_prev only when N == N_prev;
  * no other output may overlap an input.  N == 0 still commits (S_new is
  * written, o and U are empty).
  */
-treewy_status treewy_commit_verify(const float *S_old, const float *U_prev, const void *k_prev,
+treewy_status treewy_commit_verify(const void *S_old, const float *U_prev, const void *k_prev,
                                    const float *alpha_prev, const int32_t *path,
                                    const int32_t *path_len, int L_max, const int32_t *parent_prev,
                                    int N_prev, const void *q, const void *k, const void *v,
                                    const float *alpha, const float *beta, const int32_t *parent,
                                    int N, int B, int H, int d_k, int d_v, treewy_dtype in_dtype,
-                                   float *S_new, void *o, float *U, int32_t *err, void *stream);
+                                   treewy_dtype state_dtype, void *S_new, void *o, float *U, int32_t *err,
+                                   void *stream);
 
 /*
  * treewy_snapshot_verify - full-state-snapshotting baseline (Section "The
  * memory problem", approach (i)): runs eq. 1 node by node and writes every
  * node's full state, so that commit is a copy of one snapshot.  Same inputs
- * and outputs as treewy_verify except:
+ * and outputs as treewy_verify with a float32 state (no state_dtype), except:
  *   snapshots [B, H, N, d_v, d_k] float32  written: S_t of every node
  * The speculative memory is N full states per unit instead of U.
  */

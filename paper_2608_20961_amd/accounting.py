@@ -65,25 +65,27 @@ def elem_bytes(in_dtype: str) -> int:
     return {"bf16": 2, "f32": 4}[in_dtype]
 
 
-def verify_bytes(w: Workload) -> int:
+def verify_bytes(w: Workload, state_bytes: int = 4) -> int:
+    """state_bytes: 4 for a float32 state, 2 for a bfloat16 state."""
     s, d, N = elem_bytes(w.in_dtype), w.d_k, w.N
-    per_unit = d * d * 4 + 3 * N * d * s + 2 * N * 4 + N * d * s + N * d * 4
+    per_unit = d * d * state_bytes + 3 * N * d * s + 2 * N * 4 + N * d * s + N * d * 4
     return w.units * per_unit + w.B * N * 4
 
 
-def commit_bytes(w: Workload, path_len: np.ndarray) -> int:
+def commit_bytes(w: Workload, path_len: np.ndarray, state_bytes: int = 4) -> int:
     """path_len [B]: the accepted path length of every sequence."""
     s, d = elem_bytes(w.in_dtype), w.d_k
     L = np.asarray(path_len, dtype=np.int64)
-    per_seq = w.H * (2 * d * d * 4 + L * (d * 4 + d * s + 4)) + L * 4 + 4
+    per_seq = w.H * (2 * d * d * state_bytes + L * (d * 4 + d * s + 4)) + L * 4 + 4
     return int(per_seq.sum())
 
 
-def commit_verify_bytes(w: Workload, path_len: np.ndarray) -> int:
+def commit_verify_bytes(w: Workload, path_len: np.ndarray, state_bytes: int = 4) -> int:
     """The previous round's commit fused into this round's verify (both rounds
     shaped like `w`): commit + verify minus the second read of the state,
     which the fused call takes from registers."""
-    return verify_bytes(w) + commit_bytes(w, path_len) - w.units * w.d_k * w.d_v * 4
+    return (verify_bytes(w, state_bytes) + commit_bytes(w, path_len, state_bytes)
+            - w.units * w.d_k * w.d_v * state_bytes)
 
 
 def snapshot_verify_bytes(w: Workload) -> int:

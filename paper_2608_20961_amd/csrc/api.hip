@@ -14,6 +14,13 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 treewy_status hip_status(hipError_t e) { return e == hipSuccess ? TREEWY_OK : TREEWY_ERR_HIP; }
 
 // Shared checks for the calls that take the full verify inputs.
+// The state is fp32, or bf16 with bf16 inputs.
+treewy_status check_state(treewy_dtype state, treewy_dtype in) {
+    if (state != TREEWY_F32 && state != TREEWY_BF16) return TREEWY_ERR_INVALID_ARG;
+    if (state == TREEWY_BF16 && in != TREEWY_BF16) return TREEWY_ERR_UNSUPPORTED;
+    return TREEWY_OK;
+}
+
 treewy_status check_common(int N, int B, int H, int d_k, int d_v, treewy_dtype dt) {
     if (B < 0 || H < 0 || N < 0) return TREEWY_ERR_INVALID_ARG;
     if (dt != TREEWY_F32 && dt != TREEWY_BF16) return TREEWY_ERR_INVALID_ARG;
@@ -27,11 +34,12 @@ treewy_status check_common(int N, int B, int H, int d_k, int d_v, treewy_dtype d
 
 extern "C" {
 
-treewy_status treewy_verify(const float *S0, const void *q, const void *k, const void *v,
+treewy_status treewy_verify(const void *S0, const void *q, const void *k, const void *v,
                             const float *alpha, const float *beta, const int32_t *parent, int N,
-                            int B, int H, int d_k, int d_v, treewy_dtype in_dtype, void *o, float *U,
-                            int32_t *err, void *stream) {
+                            int B, int H, int d_k, int d_v, treewy_dtype in_dtype, treewy_dtype state_dtype,
+                            void *o, float *U, int32_t *err, void *stream) {
     treewy_status st = check_common(N, B, H, d_k, d_v, in_dtype);
+    if (st == TREEWY_OK) st = check_state(state_dtype, in_dtype);
     if (st != TREEWY_OK) return st;
     if (N == 0 || B == 0 || H == 0) return TREEWY_OK;
     if (!S0 || !q || !k || !v || !alpha || !beta || !parent || !o || !U) return TREEWY_ERR_INVALID_ARG;
@@ -39,15 +47,17 @@ treewy_status treewy_verify(const float *S0, const void *q, const void *k, const
         !aligned16(U))
         return TREEWY_ERR_INVALID_ARG;
     return hip_status(treewy::launch_verify(S0, q, k, v, alpha, beta, parent, N, B, H,
-                                            in_dtype == TREEWY_F32, o, U, err,
+                                            in_dtype == TREEWY_F32, state_dtype == TREEWY_BF16, o, U, err,
                                             static_cast<hipStream_t>(stream)));
 }
 
-treewy_status treewy_commit(const float *S0, const float *U, const void *k, const float *alpha,
+treewy_status treewy_commit(const void *S0, const float *U, const void *k, const float *alpha,
                             const int32_t *path, const int32_t *path_len, int L_max,
                             const int32_t *parent, int N, int B, int H, int d_k, int d_v,
-                            treewy_dtype k_dtype, float *S_new, int32_t *err, void *stream) {
+                            treewy_dtype k_dtype, treewy_dtype state_dtype, void *S_new, int32_t *err,
+                            void *stream) {
     treewy_status st = check_common(N, B, H, d_k, d_v, k_dtype);
+    if (st == TREEWY_OK && state_dtype != TREEWY_F32 && state_dtype != TREEWY_BF16) st = TREEWY_ERR_INVALID_ARG;
     if (st != TREEWY_OK) return st;
     if (L_max < 0) return TREEWY_ERR_INVALID_ARG;
     if (L_max > kMaxN) return TREEWY_ERR_UNSUPPORTED;
@@ -57,18 +67,20 @@ treewy_status treewy_commit(const float *S0, const float *U, const void *k, cons
     if (L_max > 0 && !path) return TREEWY_ERR_INVALID_ARG;
     if (!aligned16(S0) || !aligned16(S_new)) return TREEWY_ERR_INVALID_ARG;
     return hip_status(treewy::launch_commit(S0, U, k, alpha, path, path_len, L_max, parent, N, B, H,
-                                            k_dtype == TREEWY_F32, S_new, err,
+                                            k_dtype == TREEWY_F32, state_dtype == TREEWY_BF16, S_new, err,
                                             static_cast<hipStream_t>(stream)));
 }
 
-treewy_status treewy_commit_verify(const float *S_old, const float *U_prev, const void *k_prev,
+treewy_status treewy_commit_verify(const void *S_old, const float *U_prev, const void *k_prev,
                                    const float *alpha_prev, const int32_t *path,
                                    const int32_t *path_len, int L_max, const int32_t *parent_prev,
                                    int N_prev, const void *q, const void *k, const void *v,
                                    const float *alpha, const float *beta, const int32_t *parent,
                                    int N, int B, int H, int d_k, int d_v, treewy_dtype in_dtype,
-                                   float *S_new, void *o, float *U, int32_t *err, void *stream) {
+                                   treewy_dtype state_dtype, void *S_new, void *o, float *U, int32_t *err,
+                                   void *stream) {
     treewy_status st = check_common(N, B, H, d_k, d_v, in_dtype);
+    if (st == TREEWY_OK) st = check_state(state_dtype, in_dtype);
     if (st != TREEWY_OK) return st;
     if (N_prev < 0 || L_max < 0) return TREEWY_ERR_INVALID_ARG;
     if (N_prev > kMaxN || L_max > kMaxN) return TREEWY_ERR_UNSUPPORTED;
@@ -85,8 +97,8 @@ treewy_status treewy_commit_verify(const float *S_old, const float *U_prev, cons
     if (N > 0 && U == U_prev && N != N_prev) return TREEWY_ERR_INVALID_ARG;
     return hip_status(treewy::launch_commit_verify(S_old, U_prev, k_prev, alpha_prev, path, path_len, L_max,
                                                    parent_prev, N_prev, q, k, v, alpha, beta, parent, N, B,
-                                                   H, in_dtype == TREEWY_F32, S_new, o, U, err,
-                                                   static_cast<hipStream_t>(stream)));
+                                                   H, in_dtype == TREEWY_F32, state_dtype == TREEWY_BF16, S_new,
+                                                   o, U, err, static_cast<hipStream_t>(stream)));
 }
 
 treewy_status treewy_snapshot_verify(const float *S0, const void *q, const void *k, const void *v,

@@ -3,11 +3,14 @@
 // with g_a the product of alpha along the path and w_l = g_a / g_{path_l} the
 // product of alpha over the path nodes after path_l.
 //
-// One workgroup per (sequence, head) streams its 64 KiB state: every thread
-// owns sixteen float4s at stride 4 KiB, so each load and store instruction of
-// the workgroup covers 4 KiB of contiguous HBM.  The path's scaled pseudo-value
-// rows and keys (at most 64 x 128 each) are staged in LDS.  Each thread reads
-// and writes only its own elements, so S_new may alias S0.
+// One workgroup per (sequence, head) streams its state: every thread owns
+// sixteen 16-byte chunks at stride 4 KiB (an fp32 state: 4 entries each; a
+// bf16 state: 8 entries, read and written in eight chunks), so each load and
+// store instruction of the workgroup covers 4 KiB of contiguous HBM.  A bf16
+// state is updated in fp32 and rounded to nearest even on the way out.  The
+// path's scaled pseudo-value rows and keys (at most 64 x 128 each) are staged
+// in LDS.  Each thread reads and writes only its own elements, so S_new may
+// alias S0.
 #include "device.h"
 #include "launch.h"
 
@@ -15,12 +18,15 @@ namespace treewy {
 
 constexpr int MAX_PATH = 64;
 
-template <bool F32K>
+template <bool F32K, bool SBF>
 __global__ __launch_bounds__(THREADS) void commit_kernel(
-    const float *S0, const float *__restrict__ U, const void *__restrict__ k_,
+    const void *S0, const float *__restrict__ U, const void *__restrict__ k_,
     const float *__restrict__ alpha, const int32_t *__restrict__ path,
     const int32_t *__restrict__ path_len, int L_max, const int32_t *__restrict__ parent, int N,
-    int H, float *S_new, int32_t *__restrict__ err) {
+    int H, void *S_new, int32_t *__restrict__ err) {
+    constexpr int SB = SBF ? 2 : 4;                      // bytes per state entry
+    constexpr int CH = 16 / SB;                          // entries per 16-byte chunk
+    constexpr int NCH = D * D / CH / THREADS;            // chunks per thread
     using In = typename std::conditional<F32K, float, __bf16>::type;
     extern __shared__ __attribute__((aligned(16))) float stage[];   // Uw [L_max][D], Kp [L_max][D]
     __shared__ int s_node[MAX_PATH];
@@ -33,10 +39,10 @@ __global__ __launch_bounds__(THREADS) void commit_kernel(
     const size_t node0 = (size_t)u * N;
 
     // The state is touched once: stream it past the caches on the way in and out.
-    const rsrc_t rs = make_rsrc(S0 + (size_t)u * D * D, D * D * 4);
-    f32x4 s[16];
+    const rsrc_t rs = make_rsrc(static_cast<const char *>(S0) + (size_t)u * D * D * SB, D * D * SB);
+    uint4 raw[NCH];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) s[i] = ld_f32x4<STREAM>(rs, (tid + THREADS * i) * 16);
+    for (int i = 0; i < NCH; ++i) raw[i] = ld_u32x4<STREAM>(rs, (tid + THREADS * i) * 16);
 
     if (tid == 0) {
         const int len = path_len[b];
@@ -72,33 +78,68 @@ __global__ __launch_bounds__(THREADS) void commit_kernel(
     }
     __syncthreads();
 
+    // Chunk i of this thread holds row r0 + (THREADS / (D / CH)) i, entries [c0, c0 + CH).
     const float w0 = s_w0;
-    const int r0 = tid >> 5, c4 = (tid & 31) * 4;
+    const int r0 = tid / (D / CH), c0 = (tid % (D / CH)) * CH;
+    constexpr int RSTEP = THREADS / (D / CH);
+    float x[NCH][CH];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) s[i] *= w0;
+    for (int i = 0; i < NCH; ++i) {
+        if constexpr (SBF) {
+            const bf16x8 h = __builtin_bit_cast(bf16x8, raw[i]);
+#pragma unroll
+            for (int e = 0; e < CH; ++e) x[i][e] = w0 * (float)h[e];
+        } else {
+            const f32x4 f = __builtin_bit_cast(f32x4, raw[i]);
+#pragma unroll
+            for (int e = 0; e < CH; ++e) x[i][e] = w0 * f[e];
+        }
+    }
     for (int l = 0; l < len; ++l) {
-        const f32x4 kk = *reinterpret_cast<const f32x4 *>(Kp + l * D + c4);
+        float kk[CH];
+#pragma unroll
+        for (int e = 0; e < CH; e += 4) *reinterpret_cast<f32x4 *>(kk + e) = *reinterpret_cast<const f32x4 *>(Kp + l * D + c0 + e);
         const float *uw = Uw + l * D + r0;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) s[i] += uw[8 * i] * kk;
-    }
-    const rsrc_t rd = make_rsrc(S_new + (size_t)u * D * D, D * D * 4);
+        for (int i = 0; i < NCH; ++i) {
+            const float a = uw[RSTEP * i];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) st_u32x4<STREAM>(rd, (tid + THREADS * i) * 16, __builtin_bit_cast(uint4, s[i]));
+            for (int e = 0; e < CH; ++e) x[i][e] += a * kk[e];
+        }
+    }
+    const rsrc_t rd = make_rsrc(static_cast<char *>(S_new) + (size_t)u * D * D * SB, D * D * SB);
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+        uint4 out;
+        if constexpr (SBF) {
+            bf16x8 h;
+#pragma unroll
+            for (int e = 0; e < CH; ++e) h[e] = (__bf16)x[i][e];
+            out = __builtin_bit_cast(uint4, h);
+        } else {
+            out = __builtin_bit_cast(uint4, f32x4{x[i][0], x[i][1], x[i][2], x[i][3]});
+        }
+        st_u32x4<STREAM>(rd, (tid + THREADS * i) * 16, out);
+    }
 }
 
-hipError_t launch_commit(const float *S0, const float *U, const void *k, const float *alpha,
+hipError_t launch_commit(const void *S0, const float *U, const void *k, const float *alpha,
                          const int32_t *path, const int32_t *path_len, int L_max,
-                         const int32_t *parent, int N, int B, int H, bool f32_k, float *S_new,
-                         int32_t *err, hipStream_t stream) {
+                         const int32_t *parent, int N, int B, int H, bool f32_k, bool bf16_state,
+                         void *S_new, int32_t *err, hipStream_t stream) {
     const dim3 grid((unsigned)(B * H)), block(THREADS);
     const size_t lds = (size_t)2 * L_max * D * sizeof(float);
-    if (f32_k)
-        hipLaunchKernelGGL((commit_kernel<true>), grid, block, lds, stream, S0, U, k, alpha, path,
-                           path_len, L_max, parent, N, H, S_new, err);
-    else
-        hipLaunchKernelGGL((commit_kernel<false>), grid, block, lds, stream, S0, U, k, alpha, path,
-                           path_len, L_max, parent, N, H, S_new, err);
+#define TREEWY_COMMIT(F, S)                                                                                   \
+    hipLaunchKernelGGL((commit_kernel<F, S>), grid, block, lds, stream, S0, U, k, alpha, path, path_len, L_max, \
+                       parent, N, H, S_new, err)
+    if (f32_k) {
+        if (bf16_state) TREEWY_COMMIT(true, true);
+        else TREEWY_COMMIT(true, false);
+    } else {
+        if (bf16_state) TREEWY_COMMIT(false, true);
+        else TREEWY_COMMIT(false, false);
+    }
+#undef TREEWY_COMMIT
     return hipGetLastError();
 }
 

@@ -67,6 +67,9 @@ template <int P = CACHED> __device__ __forceinline__ f32x4 ld_f32x4(rsrc_t r, in
 template <int P = CACHED> __device__ __forceinline__ uint4 ld_u32x4(rsrc_t r, int off) {
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, P));
 }
+template <int P = CACHED> __device__ __forceinline__ uint2 ld_u32x2(rsrc_t r, int off) {
+    return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, P));
+}
 __device__ __forceinline__ float ld_f32(rsrc_t r, int off) {
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }
@@ -83,6 +86,10 @@ template <int P = CACHED> __device__ __forceinline__ void st_u32x4(rsrc_t r, int
     __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned int, x),
                                            r, off, 0, P);
 }
+template <int P = CACHED> __device__ __forceinline__ void st_u32x2(rsrc_t r, int off, uint2 x) {
+    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(__attribute__((ext_vector_type(2))) unsigned int, x),
+                                          r, off, 0, P);
+}
 template <int P = CACHED> __device__ __forceinline__ void st_f32(rsrc_t r, int off, float x) {
     __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned int, x), r, off, 0, P);
 }
@@ -91,6 +98,19 @@ template <int P = CACHED> __device__ __forceinline__ void st_f32(rsrc_t r, int o
 __device__ __forceinline__ int opaque(int x) {
     asm volatile("" : "+v"(x));
     return x;
+}
+
+// Four bf16 held in a uint2 <-> four floats (exact widening; narrowing rounds
+// to nearest even).
+__device__ __forceinline__ f32x4 bf4_to_f32(uint2 x) {
+    const bf16x4 h = __builtin_bit_cast(bf16x4, x);
+    return f32x4{(float)h[0], (float)h[1], (float)h[2], (float)h[3]};
+}
+__device__ __forceinline__ uint2 f32_to_bf4(f32x4 x) {
+    bf16x4 h;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) h[e] = (__bf16)x[e];
+    return __builtin_bit_cast(uint2, h);
 }
 
 __device__ __forceinline__ float to_f32(float x) { return x; }

@@ -7,23 +7,23 @@
 
 namespace treewy {
 
-hipError_t launch_verify(const float *S0, const void *q, const void *k, const void *v,
+hipError_t launch_verify(const void *S0, const void *q, const void *k, const void *v,
                          const float *alpha, const float *beta, const int32_t *parent, int N,
-                         int B, int H, bool f32_in, void *o, float *U, int32_t *err,
+                         int B, int H, bool f32_in, bool bf16_state, void *o, float *U, int32_t *err,
                          hipStream_t stream);
 
 // Commit of the previous round's accepted path fused into this round's verify.
-hipError_t launch_commit_verify(const float *S_old, const float *U_prev, const void *k_prev,
+hipError_t launch_commit_verify(const void *S_old, const float *U_prev, const void *k_prev,
                                 const float *alpha_prev, const int32_t *path, const int32_t *path_len,
                                 int L_max, const int32_t *parent_prev, int N_prev, const void *q,
                                 const void *k, const void *v, const float *alpha, const float *beta,
-                                const int32_t *parent, int N, int B, int H, bool f32_in, float *S_new,
-                                void *o, float *U, int32_t *err, hipStream_t stream);
+                                const int32_t *parent, int N, int B, int H, bool f32_in, bool bf16_state,
+                                void *S_new, void *o, float *U, int32_t *err, hipStream_t stream);
 
-hipError_t launch_commit(const float *S0, const float *U, const void *k, const float *alpha,
+hipError_t launch_commit(const void *S0, const float *U, const void *k, const float *alpha,
                          const int32_t *path, const int32_t *path_len, int L_max,
-                         const int32_t *parent, int N, int B, int H, bool f32_k, float *S_new,
-                         int32_t *err, hipStream_t stream);
+                         const int32_t *parent, int N, int B, int H, bool f32_k, bool bf16_state,
+                         void *S_new, int32_t *err, hipStream_t stream);
 
 hipError_t launch_snapshot_verify(const float *S0, const void *q, const void *k, const void *v,
                                   const float *alpha, const float *beta, const int32_t *parent,

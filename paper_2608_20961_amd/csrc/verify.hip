@@ -49,7 +49,7 @@ struct CommitArgs {
     const int32_t *path;      // [B, L_max] root -> accepted node
     const int32_t *path_len;  // [B]
     const int32_t *parent;    // [B, N_prev] or null (then only range and order are checked)
-    float *S_new;             // [units, D, D]; may be S_old
+    void *S_new;              // [units, D, D] in the state dtype; may be S_old
     int L_max, N_prev;
 };
 
@@ -95,7 +95,7 @@ struct VerifyLds {
 // One unit's HBM reads, held in registers from issue to use.  Every read goes
 // through a buffer descriptor bounded to this unit's rows, so rows of padding
 // nodes (t >= N) read as zero.
-template <int NP, bool F32IN, bool FUSE = false>
+template <int NP, bool F32IN, bool FUSE = false, bool SBF = false>
 struct UnitReads {
     using In = typename std::conditional<F32IN, float, __bf16>::type;
     static constexpr int MT = NP / 32;
@@ -107,7 +107,10 @@ struct UnitReads {
     int par;                                            // wave 0, node = lane
     float al, be;
     uint4 kq[KQN];                                      // chunk i: row (tid / CPR + i THREADS / CPR) mod NP
-    f32x4 s0[8][2];                                     // S0 row `col`, d_k 16s + 8h + 4hg + [0, 4)
+    // S0 row `col`, d_k 16s + 8h + 4hg + [0, 4): four floats, or four bf16 in a uint2 for a bf16 state
+    using SReg = typename std::conditional<SBF, uint2, f32x4>::type;
+    static constexpr int SB = SBF ? 2 : 4;              // bytes per state entry
+    SReg s0[8][2];
     static constexpr int VQN = NP * ROW / 16 / THREADS;  // V chunks per thread
     uint4 vq[VQN];                                      // V rows, 16 bytes per chunk, coalesced
     int cp_len, cp_node, cp_par;                        // fused commit, wave 1: path (lane l = entry l)
@@ -133,7 +136,16 @@ struct UnitReads {
     }
 
     // Every HBM read of unit u, in the order the unit consumes them.
-    __device__ __forceinline__ void issue(const float *S0, const In *q, const In *k, const In *vv,
+    __device__ __forceinline__ f32x4 sget(int s, int h) const {
+        if constexpr (SBF) return bf4_to_f32(s0[s][h]);
+        else return s0[s][h];
+    }
+    __device__ __forceinline__ void sset(int s, int h, f32x4 x) {
+        if constexpr (SBF) s0[s][h] = f32_to_bf4(x);
+        else s0[s][h] = x;
+    }
+
+    __device__ __forceinline__ void issue(const void *S0, const In *q, const In *k, const In *vv,
                                           const float *alpha, const float *beta, const int32_t *parent,
                                           int u, int b, int N, int tid, int lane, int wave, int hg,
                                           int col) {
@@ -154,25 +166,32 @@ struct UnitReads {
         const rsrc_t rv = make_rsrc(vv + node0 * D, N * ROW);
 #pragma unroll
         for (int i = 0; i < VQN; ++i) vq[i] = ld_u32x4<STREAM>(rv, (tid + THREADS * i) * 16);
-        const rsrc_t rs = make_rsrc(S0 + (size_t)u * D * D, D * D * 4);
-        const int base = (col * D + 4 * hg) * 4;
+        const rsrc_t rs = make_rsrc(static_cast<const char *>(S0) + (size_t)u * D * D * SB, D * D * SB);
+        const int base = (col * D + 4 * hg) * SB;
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
-            s0[s][0] = ld_f32x4<CACHED>(rs, base + 64 * s);        // d_k 16s + 4hg + [0, 4)
-            s0[s][1] = ld_f32x4<CACHED>(rs, base + 64 * s + 32);   // d_k 16s + 8 + 4hg + [0, 4)
+            if constexpr (SBF) {
+                s0[s][0] = ld_u32x2<CACHED>(rs, base + 32 * s);        // d_k 16s + 4hg + [0, 4)
+                s0[s][1] = ld_u32x2<CACHED>(rs, base + 32 * s + 16);   // d_k 16s + 8 + 4hg + [0, 4)
+            } else {
+                s0[s][0] = ld_f32x4<CACHED>(rs, base + 64 * s);
+                s0[s][1] = ld_f32x4<CACHED>(rs, base + 64 * s + 32);
+            }
         }
     }
 };
 
-template <int NP, bool F32IN, bool FUSE>
+template <int NP, bool F32IN, bool FUSE, bool SBF>
 __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_kernel(
-    const float *S0, const void *__restrict__ q_, const void *__restrict__ k_,
+    const void *S0, const void *__restrict__ q_, const void *__restrict__ k_,
     const void *__restrict__ v_, const float *__restrict__ alpha, const float *__restrict__ beta,
     const int32_t *__restrict__ parent, int N, int H, int units, void *__restrict__ o_,
     float *U, int32_t *__restrict__ err, CommitArgs cm) {
     using In = typename std::conditional<F32IN, float, __bf16>::type;
+    static_assert(!(SBF && F32IN), "a bf16 state is paired with bf16 inputs");
     using L = VerifyLds<NP, F32IN, FUSE>;
-    using Reads = UnitReads<NP, F32IN, FUSE>;
+    using Reads = UnitReads<NP, F32IN, FUSE, SBF>;
+    constexpr int SB = Reads::SB;
     constexpr int MT = NP / 32;                          // 32-row tiles of nodes
     constexpr int XS = L::XS, MS = L::MS, US = L::US, OS = L::OS;
     constexpr int CHUNK = Reads::CHUNK, CPR = Reads::CPR, KQN = Reads::KQN;
@@ -510,14 +529,19 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                     const f32x16 d = rank_block(jb, f32x16{});
 #pragma unroll
                     for (int r = 0; r < 16; ++r) {
-                        const float x = rd.s0[2 * jb + (r >> 3)][(r >> 2) & 1][r & 3];
-                        rd.s0[2 * jb + (r >> 3)][(r >> 2) & 1][r & 3] = l0 == 0 ? fmaf(ga, x, d[r]) : x + d[r];
+                        if ((r & 3) != 0) continue;             // four entries at a time
+                        const int s2 = 2 * jb + (r >> 3), h = (r >> 2) & 1;
+                        f32x4 x = rd.sget(s2, h);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) x[i] = l0 == 0 ? fmaf(ga, x[i], d[r + i]) : x[i] + d[r + i];
+                        rd.sset(s2, h, x);
                     }
                 }
             }
         }
-        const rsrc_t rn = make_rsrc(FUSE ? cm.S_new + (size_t)u * D * D : nullptr, FUSE ? D * D * 4 : 0);
-        const int sbase = (col * D + 4 * hg) * 4;
+        const rsrc_t rn = make_rsrc(FUSE ? static_cast<char *>(cm.S_new) + (size_t)u * D * D * SB : nullptr,
+                                    FUSE ? D * D * SB : 0);
+        const int sbase = (col * D + 4 * hg) * SB;
         const bool shallow = *shallow_s != 0;
         // ---- phase 3a: rows of T = (I + B)^{-1} for shallow trees ----------
         // (T (I + B))[t, j] = 0 for j != t gives, walking t's ancestors j from
@@ -589,24 +613,35 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                     if (upd_in_p) {
                         if ((s & 1) == 0) dcur = rank_block(s >> 1, f32x16{});
 #pragma unroll
-                        for (int h = 0; h < 2; ++h)
+                        for (int h = 0; h < 2; ++h) {
+                            f32x4 x = rd.sget(s, h);
 #pragma unroll
-                            for (int i = 0; i < 4; ++i)
-                                rd.s0[s][h][i] = fmaf(ga, rd.s0[s][h][i], dcur[8 * (s & 1) + 4 * h + i]);
+                            for (int i = 0; i < 4; ++i) x[i] = fmaf(ga, x[i], dcur[8 * (s & 1) + 4 * h + i]);
+                            rd.sset(s, h, x);                   // a bf16 state is rounded here, then used
+                        }
                     }
 #pragma unroll
-                    for (int h = 0; h < 2; ++h)
-                        st_u32x4<CACHED>(rn, sbase + 64 * s + 32 * h, __builtin_bit_cast(uint4, rd.s0[s][h]));
+                    for (int h = 0; h < 2; ++h) {
+                        if constexpr (SBF)
+                            st_u32x2<CACHED>(rn, sbase + 32 * s + 16 * h, rd.s0[s][h]);
+                        else
+                            st_u32x4<CACHED>(rn, sbase + 64 * s + 32 * h, __builtin_bit_cast(uint4, rd.s0[s][h]));
+                    }
                 }
-                float sv[8];
-                *reinterpret_cast<f32x4 *>(sv) = rd.s0[s][0];
-                *reinterpret_cast<f32x4 *>(sv + 4) = rd.s0[s][1];
                 bf16x8 bh, bl;
-                split8(sv, bh, bl);
+                if constexpr (SBF) {                     // a bf16 state is exact on the matrix cores
+                    bh = __builtin_bit_cast(bf16x8, make_uint4(rd.s0[s][0].x, rd.s0[s][0].y, rd.s0[s][1].x,
+                                                               rd.s0[s][1].y));
+                } else {
+                    float sv[8];
+                    *reinterpret_cast<f32x4 *>(sv) = rd.s0[s][0];
+                    *reinterpret_cast<f32x4 *>(sv + 4) = rd.s0[s][1];
+                    split8(sv, bh, bl);
+                }
 #pragma unroll
                 for (int m = 0; m < 2 * MT; ++m) {
                     accp[m] = mma(afr[s % NBUF][m], bh, accp[m]);
-                    accp[m] = mma(afr[s % NBUF][m], bl, accp[m]);
+                    if constexpr (!SBF) accp[m] = mma(afr[s % NBUF][m], bl, accp[m]);
                     if constexpr (F32IN) accp[m] = mma(alo[s % NBUF][m], bh, accp[m]);
                 }
                 __builtin_amdgcn_sched_barrier(0);
@@ -744,7 +779,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 
 namespace {
 
-template <int NP, bool F32IN, bool FUSE>
+template <int NP, bool F32IN, bool FUSE, bool SBF>
 int resident_grid(int units) {
     static int per_device[64] = {0};
     int dev = 0;
@@ -753,53 +788,59 @@ int resident_grid(int units) {
         int cus = 0, blocks = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
             cus = 256;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, verify_kernel<NP, F32IN, FUSE>, THREADS, 0) !=
-                hipSuccess || blocks <= 0)
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, verify_kernel<NP, F32IN, FUSE, SBF>, THREADS,
+                                                         0) != hipSuccess ||
+            blocks <= 0)
             blocks = 1;
         per_device[dev] = cus * blocks;
     }
     return units < per_device[dev] ? units : per_device[dev];
 }
 
-template <int NP, bool F32IN, bool FUSE>
-hipError_t launch(const float *S0, const void *q, const void *k, const void *v, const float *alpha,
+template <int NP, bool F32IN, bool FUSE, bool SBF>
+hipError_t launch(const void *S0, const void *q, const void *k, const void *v, const float *alpha,
                   const float *beta, const int32_t *parent, int N, int B, int H, void *o, float *U,
                   int32_t *err, const CommitArgs &cm, hipStream_t stream) {
     const int units = B * H;
-    hipLaunchKernelGGL((verify_kernel<NP, F32IN, FUSE>), dim3((unsigned)resident_grid<NP, F32IN, FUSE>(units)),
-                       dim3(THREADS), 0, stream, S0, q, k, v, alpha, beta, parent, N, H, units, o, U, err, cm);
+    hipLaunchKernelGGL((verify_kernel<NP, F32IN, FUSE, SBF>),
+                       dim3((unsigned)resident_grid<NP, F32IN, FUSE, SBF>(units)), dim3(THREADS), 0, stream, S0, q,
+                       k, v, alpha, beta, parent, N, H, units, o, U, err, cm);
     return hipGetLastError();
 }
 
+// fp32 inputs pair with an fp32 state (the caller checks); a bf16 state with bf16 inputs.
 template <bool FUSE>
-hipError_t dispatch(const float *S0, const void *q, const void *k, const void *v, const float *alpha,
-                    const float *beta, const int32_t *parent, int N, int B, int H, bool f32_in, void *o,
-                    float *U, int32_t *err, const CommitArgs &cm, hipStream_t stream) {
+hipError_t dispatch(const void *S0, const void *q, const void *k, const void *v, const float *alpha,
+                    const float *beta, const int32_t *parent, int N, int B, int H, bool f32_in, bool bf16_state,
+                    void *o, float *U, int32_t *err, const CommitArgs &cm, hipStream_t stream) {
+    if (bf16_state)
+        return N <= 32 ? launch<32, false, FUSE, true>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream)
+                       : launch<64, false, FUSE, true>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream);
     if (N <= 32)
-        return f32_in ? launch<32, true, FUSE>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream)
-                      : launch<32, false, FUSE>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream);
-    return f32_in ? launch<64, true, FUSE>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream)
-                  : launch<64, false, FUSE>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream);
+        return f32_in ? launch<32, true, FUSE, false>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream)
+                      : launch<32, false, FUSE, false>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream);
+    return f32_in ? launch<64, true, FUSE, false>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream)
+                  : launch<64, false, FUSE, false>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream);
 }
 
 }  // namespace
 
-hipError_t launch_verify(const float *S0, const void *q, const void *k, const void *v,
+hipError_t launch_verify(const void *S0, const void *q, const void *k, const void *v,
                          const float *alpha, const float *beta, const int32_t *parent, int N,
-                         int B, int H, bool f32_in, void *o, float *U, int32_t *err,
+                         int B, int H, bool f32_in, bool bf16_state, void *o, float *U, int32_t *err,
                          hipStream_t stream) {
     const CommitArgs none = {};
-    return dispatch<false>(S0, q, k, v, alpha, beta, parent, N, B, H, f32_in, o, U, err, none, stream);
+    return dispatch<false>(S0, q, k, v, alpha, beta, parent, N, B, H, f32_in, bf16_state, o, U, err, none, stream);
 }
 
-hipError_t launch_commit_verify(const float *S_old, const float *U_prev, const void *k_prev,
+hipError_t launch_commit_verify(const void *S_old, const float *U_prev, const void *k_prev,
                                 const float *alpha_prev, const int32_t *path, const int32_t *path_len,
                                 int L_max, const int32_t *parent_prev, int N_prev, const void *q,
                                 const void *k, const void *v, const float *alpha, const float *beta,
-                                const int32_t *parent, int N, int B, int H, bool f32_in, float *S_new,
-                                void *o, float *U, int32_t *err, hipStream_t stream) {
+                                const int32_t *parent, int N, int B, int H, bool f32_in, bool bf16_state,
+                                void *S_new, void *o, float *U, int32_t *err, hipStream_t stream) {
     const CommitArgs cm = {U_prev, k_prev, alpha_prev, path, path_len, parent_prev, S_new, L_max, N_prev};
-    return dispatch<true>(S_old, q, k, v, alpha, beta, parent, N, B, H, f32_in, o, U, err, cm, stream);
+    return dispatch<true>(S_old, q, k, v, alpha, beta, parent, N, B, H, f32_in, bf16_state, o, U, err, cm, stream);
 }
 
 }  // namespace treewy

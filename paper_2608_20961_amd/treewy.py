@@ -38,11 +38,11 @@ TREEWY_F32, TREEWY_BF16 = 0, 1
 FLAG_BAD_PARENT, FLAG_BAD_PATH = 1, 2
 
 _P, _I = ctypes.c_void_p, ctypes.c_int
-lib.treewy_verify.argtypes = [_P] * 7 + [_I] * 6 + [_P] * 4
+lib.treewy_verify.argtypes = [_P] * 7 + [_I] * 7 + [_P] * 4
 lib.treewy_verify.restype = _I
-lib.treewy_commit.argtypes = [_P] * 6 + [_I, _P] + [_I] * 6 + [_P] * 3
+lib.treewy_commit.argtypes = [_P] * 6 + [_I, _P] + [_I] * 7 + [_P] * 3
 lib.treewy_commit.restype = _I
-lib.treewy_commit_verify.argtypes = [_P] * 6 + [_I, _P, _I] + [_P] * 6 + [_I] * 6 + [_P] * 5
+lib.treewy_commit_verify.argtypes = [_P] * 6 + [_I, _P, _I] + [_P] * 6 + [_I] * 7 + [_P] * 5
 lib.treewy_commit_verify.restype = _I
 lib.treewy_snapshot_verify.argtypes = [_P] * 7 + [_I] * 6 + [_P] * 4
 lib.treewy_snapshot_verify.restype = _I
@@ -92,6 +92,15 @@ def _need(t: torch.Tensor, name: str, dtype, shape) -> None:
         raise ValueError("%s must be contiguous" % name)
 
 
+def _state_dtype(S: torch.Tensor) -> int:
+    """float32 state, or bfloat16 state (with bfloat16 inputs; the library checks)."""
+    if S.dtype == torch.float32:
+        return TREEWY_F32
+    if S.dtype == torch.bfloat16:
+        return TREEWY_BF16
+    raise TypeError("the state must be float32 or bfloat16, got %s" % S.dtype)
+
+
 def _in_dtype(t: torch.Tensor) -> int:
     if t.dtype == torch.bfloat16:
         return TREEWY_BF16
@@ -105,7 +114,7 @@ def treewy_verify(S0, q, k, v, alpha, beta, parent, o=None, U=None, err=None, st
     B, H, N, dk = q.shape
     dv = v.shape[-1]
     dt = q.dtype
-    _need(S0, "S0", torch.float32, (B, H, dv, dk))
+    _need(S0, "S0", S0.dtype, (B, H, dv, dk))
     _need(q, "q", dt, (B, H, N, dk)); _need(k, "k", dt, (B, H, N, dk)); _need(v, "v", dt, (B, H, N, dv))
     _need(alpha, "alpha", torch.float32, (B, H, N)); _need(beta, "beta", torch.float32, (B, H, N))
     _need(parent, "parent", torch.int32, (B, N))
@@ -117,7 +126,8 @@ def treewy_verify(S0, q, k, v, alpha, beta, parent, o=None, U=None, err=None, st
     if err is not None:
         _need(err, "err", torch.int32, (B,))
     _check(lib.treewy_verify(_ptr(S0), _ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(beta), _ptr(parent),
-                             N, B, H, dk, dv, _in_dtype(q), _ptr(o), _ptr(U), _ptr(err), _stream(stream)),
+                             N, B, H, dk, dv, _in_dtype(q), _state_dtype(S0), _ptr(o), _ptr(U), _ptr(err),
+                             _stream(stream)),
            "treewy_verify")
     return o, U
 
@@ -127,19 +137,19 @@ def treewy_commit(S0, U, k, alpha, path, path_len, parent=None, S_new=None, err=
     B, H, N, dk = k.shape
     dv = U.shape[-1]
     L_max = path.shape[1]
-    _need(S0, "S0", torch.float32, (B, H, dv, dk)); _need(U, "U", torch.float32, (B, H, N, dv))
+    _need(S0, "S0", S0.dtype, (B, H, dv, dk)); _need(U, "U", torch.float32, (B, H, N, dv))
     _need(k, "k", k.dtype, (B, H, N, dk)); _need(alpha, "alpha", torch.float32, (B, H, N))
     _need(path, "path", torch.int32, (B, L_max)); _need(path_len, "path_len", torch.int32, (B,))
     if parent is not None:
         _need(parent, "parent", torch.int32, (B, N))
     if S_new is None:
         S_new = torch.empty_like(S0)
-    _need(S_new, "S_new", torch.float32, (B, H, dv, dk))
+    _need(S_new, "S_new", S0.dtype, (B, H, dv, dk))
     if err is not None:
         _need(err, "err", torch.int32, (B,))
     _check(lib.treewy_commit(_ptr(S0), _ptr(U), _ptr(k), _ptr(alpha), _ptr(path), _ptr(path_len), L_max,
-                             _ptr(parent), N, B, H, dk, dv, _in_dtype(k), _ptr(S_new), _ptr(err),
-                             _stream(stream)), "treewy_commit")
+                             _ptr(parent), N, B, H, dk, dv, _in_dtype(k), _state_dtype(S0), _ptr(S_new),
+                             _ptr(err), _stream(stream)), "treewy_commit")
     return S_new
 
 
@@ -151,7 +161,7 @@ def treewy_commit_verify(S_old, U_prev, k_prev, alpha_prev, path, path_len, q, k
     N_prev = k_prev.shape[2]
     L_max = path.shape[1]
     dt = q.dtype
-    _need(S_old, "S_old", torch.float32, (B, H, dv, dk))
+    _need(S_old, "S_old", S_old.dtype, (B, H, dv, dk))
     _need(U_prev, "U_prev", torch.float32, (B, H, N_prev, dv)); _need(k_prev, "k_prev", dt, (B, H, N_prev, dk))
     _need(alpha_prev, "alpha_prev", torch.float32, (B, H, N_prev))
     _need(path, "path", torch.int32, (B, L_max)); _need(path_len, "path_len", torch.int32, (B,))
@@ -166,14 +176,15 @@ def treewy_commit_verify(S_old, U_prev, k_prev, alpha_prev, path, path_len, q, k
         o = torch.empty((B, H, N, dv), dtype=dt, device=q.device)
     if U is None:
         U = torch.empty((B, H, N, dv), dtype=torch.float32, device=q.device)
-    _need(S_new, "S_new", torch.float32, (B, H, dv, dk))
+    _need(S_new, "S_new", S_old.dtype, (B, H, dv, dk))
     _need(o, "o", dt, (B, H, N, dv)); _need(U, "U", torch.float32, (B, H, N, dv))
     if err is not None:
         _need(err, "err", torch.int32, (B,))
     _check(lib.treewy_commit_verify(_ptr(S_old), _ptr(U_prev), _ptr(k_prev), _ptr(alpha_prev), _ptr(path),
                                     _ptr(path_len), L_max, _ptr(parent_prev), N_prev, _ptr(q), _ptr(k), _ptr(v),
                                     _ptr(alpha), _ptr(beta), _ptr(parent), N, B, H, dk, dv, _in_dtype(q),
-                                    _ptr(S_new), _ptr(o), _ptr(U), _ptr(err), _stream(stream)),
+                                    _state_dtype(S_old), _ptr(S_new), _ptr(o), _ptr(U), _ptr(err),
+                                    _stream(stream)),
            "treewy_commit_verify")
     return S_new, o, U
 

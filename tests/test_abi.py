@@ -45,7 +45,9 @@ A = ctypes.c_void_p(16)   # aligned stand-in pointers: never dereferenced by the
 M = ctypes.c_void_p(18)   # misaligned
 
 
-def _verify(tw, fn="treewy_verify", S0=A, q=A, N=8, B=2, H=2, dk=128, dv=128, dt=1, o=A, U=A):
+def _verify(tw, fn="treewy_verify", S0=A, q=A, N=8, B=2, H=2, dk=128, dv=128, dt=1, o=A, U=A, st=0):
+    if fn == "treewy_verify":
+        return tw.lib.treewy_verify(S0, q, A, A, A, A, A, N, B, H, dk, dv, dt, st, o, U, None, None)
     return getattr(tw.lib, fn)(S0, q, A, A, A, A, A, N, B, H, dk, dv, dt, o, U, None, None)
 
 
@@ -60,6 +62,9 @@ def test_verify_host_checks(tw, fn):
     assert _verify(tw, fn, S0=None) == tw.TREEWY_ERR_INVALID_ARG
     assert _verify(tw, fn, U=None) == tw.TREEWY_ERR_INVALID_ARG
     assert _verify(tw, fn, S0=M) == tw.TREEWY_ERR_INVALID_ARG
+    if fn == "treewy_verify":
+        assert _verify(tw, fn, st=2) == tw.TREEWY_ERR_INVALID_ARG
+        assert _verify(tw, fn, dt=0, st=1) == tw.TREEWY_ERR_UNSUPPORTED
     # nothing to do: returns before touching any pointer or the GPU
     assert _verify(tw, fn, N=0, S0=None) == tw.TREEWY_OK
     assert _verify(tw, fn, B=0, S0=None) == tw.TREEWY_OK
@@ -69,8 +74,8 @@ def test_verify_host_checks(tw, fn):
 def test_commit_host_checks(tw):
     f = tw.lib.treewy_commit
 
-    def call(S0=A, path=A, plen=A, L_max=8, N=8, B=2, H=2, dk=128, dt=1, S_new=A):
-        return f(S0, A, A, A, path, plen, L_max, None, N, B, H, dk, 128, dt, S_new, None, None)
+    def call(S0=A, path=A, plen=A, L_max=8, N=8, B=2, H=2, dk=128, dt=1, S_new=A, st=0):
+        return f(S0, A, A, A, path, plen, L_max, None, N, B, H, dk, 128, dt, st, S_new, None, None)
 
     assert call(dk=64) == tw.TREEWY_ERR_UNSUPPORTED
     assert call(L_max=65) == tw.TREEWY_ERR_UNSUPPORTED
@@ -79,6 +84,7 @@ def test_commit_host_checks(tw):
     assert call(path=None) == tw.TREEWY_ERR_INVALID_ARG
     assert call(S_new=M) == tw.TREEWY_ERR_INVALID_ARG
     assert call(dt=2) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(st=5) == tw.TREEWY_ERR_INVALID_ARG
     assert call(B=0, S0=None) == tw.TREEWY_OK
 
 
@@ -86,9 +92,9 @@ def test_commit_verify_host_checks(tw):
     f = tw.lib.treewy_commit_verify
 
     def call(S_old=A, U_prev=A, k_prev=A, path=A, plen=A, L_max=8, N_prev=8, q=A, N=8, B=2, H=2, dk=128,
-             dt=1, S_new=A, o=A, U=A):
+             dt=1, S_new=A, o=A, U=A, st=0):
         return f(S_old, U_prev, k_prev, A, path, plen, L_max, None, N_prev, q, A, A, A, A, A, N, B, H, dk, 128,
-                 dt, S_new, o, U, None, None)
+                 dt, st, S_new, o, U, None, None)
 
     assert call(dk=64) == tw.TREEWY_ERR_UNSUPPORTED
     assert call(N=65) == tw.TREEWY_ERR_UNSUPPORTED
@@ -97,6 +103,8 @@ def test_commit_verify_host_checks(tw):
     assert call(N_prev=-1) == tw.TREEWY_ERR_INVALID_ARG
     assert call(L_max=-1) == tw.TREEWY_ERR_INVALID_ARG
     assert call(dt=3) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(st=3) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(dt=0, st=1) == tw.TREEWY_ERR_UNSUPPORTED     # a bf16 state needs bf16 inputs
     assert call(S_old=None) == tw.TREEWY_ERR_INVALID_ARG
     assert call(plen=None) == tw.TREEWY_ERR_INVALID_ARG
     assert call(path=None) == tw.TREEWY_ERR_INVALID_ARG
