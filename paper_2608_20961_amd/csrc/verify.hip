@@ -16,8 +16,9 @@
 // core operand registers.  K and Q are staged once in LDS as bf16 and read by
 // all four waves.  T = (I + B)^{-1} has the ancestor sparsity of the tree, and
 // row t of T only involves the entries of B between t's ancestors, so each
-// lane of one wave builds one row of T independently (work ~ depth^2), in
-// place over B while the other waves start on P.  U = T R
+// lane of one wave builds one row of T independently, in place over B while
+// the other waves start on P (gathered into registers for shallow trees, a
+// dense column sweep for deep ones).  U = T R
 // and A U then run on the matrix cores with R and U taken straight from the
 // accumulator registers (the contraction index is permuted to match the
 // accumulator layout; T and A are read in the same permuted order).  U and O
@@ -85,7 +86,6 @@ struct VerifyLds {
     static constexpr int KPT_OFF = META_OFF + 2 * META_BYTES;
     static constexpr int UWT_OFF = KPT_OFF + D * CL * (F32IN ? 4 : 2);
     static constexpr int BYTES = FUSE ? UWT_OFF + D * CL * 4 : BASE_BYTES;
-    static_assert(NP * MS * 4 <= X_BYTES, "T must fit where K/Q were staged");
     static_assert(NP * US * 4 <= B_OFF, "U staging must fit where K/Q were staged");
     static_assert(B_OFF % 16 == 0 && A_OFF % 16 == 0 && BETA_OFF % 16 == 0 && G_OFF % 16 == 0 &&
                   ANC_OFF % 32 == 0 && O_OFF % 16 == 0 && V_OFF % 16 == 0 &&
@@ -181,6 +181,44 @@ struct UnitReads {
     }
 };
 
+// One column of the dense sweep that builds row t of T = (I + B)^{-1} (see
+// phase 3a), then the next column down.  Compile-time recursion keeps every
+// index into r static (r stays in registers).  Each column's row read must
+// not be hoisted far ahead (that needs a register per element of B); two
+// fences do it, whichever the compiler schedules without spilling for this
+// size: for 32 nodes the row address passes through an empty asm that also
+// takes the previous column's pivot (rows are fetched one column ahead), for
+// 64 a compiler memory barrier closes each column.
+template <int I, int NP, int MS>
+__device__ __forceinline__ void sweep_column(float (&r)[NP], const float *Bm, int t, float prev) {
+    if constexpr (I >= 0) {
+        const float x = I < t ? -r[I] : 0.f;            // T[t, I] (zero on and above the diagonal)
+        r[I] = x;
+        if constexpr (NP <= 32) {
+            int base = I * MS;
+            asm volatile("" : "+v"(base) : "v"(prev));
+            f32x4 bi[(I + 3) / 4 > 0 ? (I + 3) / 4 : 1];
+#pragma unroll
+            for (int c = 0; c < (I + 3) / 4; ++c) bi[c] = *reinterpret_cast<const f32x4 *>(Bm + base + 4 * c);
+#pragma unroll
+            for (int c = 0; c < (I + 3) / 4; ++c)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (4 * c + e < I) r[4 * c + e] = fmaf(x, bi[c][e], r[4 * c + e]);
+        } else {
+#pragma unroll
+            for (int c = 0; c < (I + 3) / 4; ++c) {
+                const f32x4 bi = *reinterpret_cast<const f32x4 *>(Bm + I * MS + 4 * c);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (4 * c + e < I) r[4 * c + e] = fmaf(x, bi[e], r[4 * c + e]);
+            }
+            asm volatile("" ::: "memory");
+        }
+        sweep_column<I - 1, NP, MS>(r, Bm, t, x);
+    }
+}
+
 template <int NP, bool F32IN, bool FUSE, bool SBF>
 __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_kernel(
     const void *S0, const void *__restrict__ q_, const void *__restrict__ k_,
@@ -201,8 +239,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
     __bf16 *Xl = reinterpret_cast<__bf16 *>(lds + L::XLO_OFF);
     float *Bm = reinterpret_cast<float *>(lds + L::B_OFF);
     float *Am = reinterpret_cast<float *>(lds + L::A_OFF);
-    float *Tm = reinterpret_cast<float *>(lds);          // T of deep trees reuses the K/Q area after P,
-    float *Us = reinterpret_cast<float *>(lds);          // then U is staged there
+    float *Us = reinterpret_cast<float *>(lds);          // U is staged where K/Q were, after P
     __bf16 *Os = reinterpret_cast<__bf16 *>(lds + L::O_OFF);   // o staging (bf16 input only)
     float *be_s = reinterpret_cast<float *>(lds + L::BETA_OFF);
     float *g_s = reinterpret_cast<float *>(lds + L::G_OFF);
@@ -543,13 +580,14 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                                     FUSE ? D * D * SB : 0);
         const int sbase = (col * D + 4 * hg) * SB;
         const bool shallow = *shallow_s != 0;
-        // ---- phase 3a: rows of T = (I + B)^{-1} for shallow trees ----------
+        // ---- phase 3a: rows of T = (I + B)^{-1}, on wave 3 while the others start on P
         // (T (I + B))[t, j] = 0 for j != t gives, walking t's ancestors j from
         // the nearest upwards, T[t, j] = -sum over i in {t} and the ancestors
-        // of t below j of T[t, i] B[i, j], with T[t, t] = 1.  T has the
-        // sparsity of B plus the diagonal, so with every entry a lane needs
-        // gathered into registers first, row t of T overwrites row t of B.
-        // One wave does it while the others start on P.
+        // of t below j of T[t, i] B[i, j], with T[t, t] = 1.  Each lane
+        // builds its own row t, which overwrites row t of B.
+        // Shallow trees (at most FAST ancestors per node): T has the sparsity
+        // of B plus the diagonal; a lane gathers the entries among its
+        // ancestors into registers first.
         if (shallow && wave == 3 && lane < NP) {
             const int t = lane;
             const uint64_t anc = t < N ? anc_s[t] : 0ull;
@@ -580,6 +618,31 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 #pragma unroll
             for (int kk = 0; kk < FAST; ++kk)
                 if (kk < m) Tt[a[kk]] = x[kk];
+        }
+        // Deeper trees: the same recurrence as a dense column sweep.  Lane t
+        // keeps r[j] = sum over the finished columns i of T[t, i] B[i, j]; at
+        // column i (from the last down) T[t, i] = -r[i] is final and row i
+        // of B (one broadcast read) is added in.  B is zero off the ancestor
+        // pattern, so the sweep reaches the same T for any tree; it costs
+        // NP^2 / 2 fused multiply-adds per lane and no dependent LDS reads.
+        // Every read of B precedes the final row stores.
+        if (!shallow && wave == 3) {
+            const int t = lane < NP ? lane : NP - 1;
+            float r[NP];
+#pragma unroll
+            for (int c = 0; c < NP / 4; ++c) {
+                const f32x4 bt = *reinterpret_cast<const f32x4 *>(Bm + t * MS + 4 * c);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) r[4 * c + e] = bt[e];
+            }
+            sweep_column<NP - 1, NP, MS>(r, Bm, t, 0.f);
+            if (lane < NP) {
+                float *Tt = Bm + t * MS;
+#pragma unroll
+                for (int c = 0; c < NP / 4; ++c)
+                    *reinterpret_cast<f32x4 *>(Tt + 4 * c) = f32x4{r[4 * c], r[4 * c + 1], r[4 * c + 2], r[4 * c + 3]};
+                if (t < N) Tt[t] = 1.f;
+            }
         }
 
         // ---- phase 3: P = [K; Q] S0^T for this wave's 32 columns ----------
@@ -649,33 +712,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         }
         __syncthreads();
 
-        // ---- phase 4: deep trees build T where K/Q were (wave 0); R and g P_Q
-        if (!shallow && wave == 0 && lane < NP) {
-            const int t = lane;
-            float *Tt = Tm + t * MS;
-            {
-                f32x4 *row = reinterpret_cast<f32x4 *>(Tt);
-#pragma unroll
-                for (int c = 0; c < MS / 4; ++c) row[c] = f32x4{0.f, 0.f, 0.f, 0.f};
-            }
-            if (t < N) {
-                Tt[t] = 1.f;
-                const uint64_t anc = anc_s[t];
-                uint64_t rem = anc;
-                while (rem) {
-                    const int j = 63 - __builtin_clzll(rem);
-                    rem &= ~(1ull << j);
-                    float acc = Bm[t * MS + j];
-                    uint64_t below = anc & ~((2ull << j) - 1ull);   // ancestors of t deeper than j
-                    while (below) {
-                        const int i = __builtin_ctzll(below);
-                        below &= below - 1;
-                        acc += Tt[i] * Bm[i * MS + j];
-                    }
-                    Tt[j] = -acc;
-                }
-            }
-        }
+        // ---- phase 4: R and g P_Q ---------------------------------------------
 #pragma unroll
         for (int m = 0; m < MT; ++m)
 #pragma unroll
@@ -696,7 +733,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // K-step s covers nodes [16s, 16s+16) in the order the accumulator
         // holds them: slot e of lane group hg is node 32(s/2) + 16(s%2) +
         // 8(e/4) + 4hg + e%4.
-        const float *Tsrc = shallow ? Bm : Tm;
+        const float *Tsrc = Bm;
         f32x16 accv[MT];
 #pragma unroll
         for (int m = 0; m < MT; ++m) accv[m] = f32x16{};
