@@ -47,6 +47,8 @@ def parse():
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-snapshot", action="store_true")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--prefill-tokens", type=int, default=1024,
+                   help="tokens per sequence for the chain-prefill measurement (0 skips it)")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time for the CPU baseline")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain 1 GiB device copy (for scaling HBM counters)")
@@ -117,11 +119,10 @@ def copy_calibration(torch):
 
 
 def device_inputs(torch, tw, wl, w, seed):
-    """Seeded inputs on the device; S0 made on the device by running verify +
-    commit over warm-up chains of 32 float32 tokens (the committed state of
-    each chunk is the next chunk's S0).  The warm-up uses the float32, N <= 32
-    kernels, so a profile's per-kernel statistics for the timed bf16 kernels
-    cover only the timed launches."""
+    """Seeded inputs on the device; S0 made on the device by the library's
+    chain prefill over the workload's warm-up tokens in float32 (the float32
+    kernels, so a profile's statistics for the timed bf16 kernels cover only
+    the timed launches)."""
     dev = torch.device("cuda:0")
     dt = torch.bfloat16 if w.in_dtype == "bf16" else torch.float32
     x = wl.make_inputs(w, seed=seed)
@@ -133,17 +134,10 @@ def device_inputs(torch, tw, wl, w, seed):
              beta=put(x["beta"], torch.float32), parent=put(x["parent"], torch.int32),
              path=put(x["path"], torch.int32), path_len=put(x["path_len"], torch.int32))
     S = torch.zeros((w.B, w.H, w.d_v, w.d_k), dtype=torch.float32, device=dev)
-    T = 32
-    chunks = (w.warm_tokens + T - 1) // T
-    for c in range(chunks):
-        Tc = min(T, w.warm_tokens - c * T)
-        k, v, a, b = wl.warmup_chunk_torch(w, seed, c, Tc, dev, torch.float32)
-        par = torch.arange(-1, Tc - 1, dtype=torch.int32, device=dev).repeat(w.B, 1).contiguous()
-        path = torch.arange(Tc, dtype=torch.int32, device=dev).repeat(w.B, 1).contiguous()
-        plen = torch.full((w.B,), Tc, dtype=torch.int32, device=dev)
-        _, U = tw.treewy_verify(S, k, k, v, a, b, par)
-        S = tw.treewy_commit(S, U, k, a, path, plen, parent=par, S_new=S)
+    k, v, a, b = wl.warmup_chunk_torch(w, seed, 0, w.warm_tokens, dev, torch.float32)
+    tw.treewy_chain_prefill(S, k, k, v, a, b, S_T=S)
     torch.cuda.synchronize()
+    del k, v, a, b
     d["S0"] = S
     return x, d
 
@@ -337,6 +331,25 @@ def main():
             "speedup_vs_f32_state": round(ms_step / ms_step_b, 3),
         }
         del S0_b, S0_bc, S_new_b, o_b, U_b, o_f2, U_f2
+    # Chain prefill (bf16 tokens, float32 state) at the workload's B x H.
+    Tp = args.prefill_tokens
+    if Tp > 0 and w.in_dtype == "bf16":
+        kp, vp, ap, bp = wl.warmup_chunk_torch(w, args.seed, 1, Tp, "cuda", torch.bfloat16)
+        qp = wl.warmup_chunk_torch(w, args.seed, 2, Tp, "cuda", torch.bfloat16)[0]
+        S_p = torch.empty_like(d["S0"])
+        o_p = torch.empty_like(vp)
+        U_p = torch.empty((2, w.B, w.H, 64, w.d_v), dtype=torch.float32, device="cuda")
+
+        def prefill():
+            tw.treewy_chain_prefill(d["S0"], qp, kp, vp, ap, bp, S_T=S_p, o=o_p, U_work=U_p)
+
+        _, (ms_pf,) = time_steps(torch, [prefill], max(3, args.steps // 10), 1)
+        pb = acc.prefill_bytes(w, Tp)
+        result["chain_prefill"] = dict(roofline(pb, ms_pf, None), tokens=Tp,
+                                       tokens_per_s=round(w.B * Tp / (ms_pf * 1e-3), 1),
+                                       launches=(Tp + 63) // 64 + 1)
+        log("chain prefill of %d tokens: %.4f ms" % (Tp, ms_pf))
+        del kp, vp, ap, bp, qp, S_p, o_p, U_p
     # Greedy acceptance on the device (tokens: vocabulary of 4, the target
     # agreeing with the drafter along one planted chain per sequence).
     tok = wl.acceptance_tokens(x["parent"], seed=args.seed, vocab=4, plant=True)

@@ -88,6 +88,13 @@ def commit_verify_bytes(w: Workload, path_len: np.ndarray, state_bytes: int = 4)
             - w.units * w.d_k * w.d_v * state_bytes)
 
 
+def prefill_bytes(w: Workload, T: int, state_bytes: int = 4) -> int:
+    """Chain prefill of T tokens per unit: the state read and written once,
+    q, k, v read and o written per token, alpha and beta per token."""
+    s, d = elem_bytes(w.in_dtype), w.d_k
+    return w.units * (2 * d * d * state_bytes + T * (4 * d * s + 2 * 4))
+
+
 def snapshot_verify_bytes(w: Workload) -> int:
     s, d, N = elem_bytes(w.in_dtype), w.d_k, w.N
     per_unit = d * d * 4 + 3 * N * d * s + 2 * N * 4 + N * d * s + N * d * d * 4

@@ -52,6 +52,9 @@ struct CommitArgs {
     const int32_t *parent;    // [B, N_prev] or null (then only range and order are checked)
     void *S_new;              // [units, D, D] in the state dtype; may be S_old
     int L_max, N_prev;
+    int in_stride;            // rows per unit in k and alpha (N_prev for whole tensors)
+    int u_stride;             // rows per unit in U (N_prev for whole tensors)
+    int chain_len;            // >= 0: the path is 0 .. chain_len - 1 of a chain (path arrays unused)
 };
 
 template <int NP, bool F32IN, bool FUSE = false>
@@ -129,9 +132,15 @@ struct UnitReads {
     // previous round's alpha and parent of node = lane.
     __device__ __forceinline__ void issue_path(const CommitArgs &cm, int u, int b, int lane) {
         const int np = cm.N_prev;
+        cp_al = ld_f32(make_rsrc(cm.alpha + (size_t)u * cm.in_stride, np * 4), lane * 4);
+        if (cm.chain_len >= 0) {                        // the whole chain: node l at entry l
+            cp_len = cm.chain_len;
+            cp_node = lane;
+            cp_par = lane - 1;
+            return;
+        }
         cp_len = ld_i32(make_rsrc(cm.path_len + b, 4), 0);
         cp_node = ld_i32(make_rsrc(cm.path + (size_t)b * cm.L_max, cm.L_max * 4), lane * 4);
-        cp_al = ld_f32(make_rsrc(cm.alpha + (size_t)u * np, np * 4), lane * 4);
         cp_par = cm.parent ? ld_i32(make_rsrc(cm.parent + (size_t)b * np, np * 4), lane * 4) : 0;
     }
 
@@ -147,11 +156,11 @@ struct UnitReads {
 
     __device__ __forceinline__ void issue(const void *S0, const In *q, const In *k, const In *vv,
                                           const float *alpha, const float *beta, const int32_t *parent,
-                                          int u, int b, int N, int tid, int lane, int wave, int hg,
-                                          int col) {
-        const size_t node0 = (size_t)u * N;
+                                          int u, int b, int N, int in_stride, int tid, int lane, int wave,
+                                          int hg, int col) {
+        const size_t node0 = (size_t)u * in_stride;
         if (wave == 0) {
-            par = ld_i32(make_rsrc(parent + (size_t)b * N, N * 4), lane * 4);
+            par = parent ? ld_i32(make_rsrc(parent + (size_t)b * N, N * 4), lane * 4) : lane - 1;
             al = ld_f32(make_rsrc(alpha + node0, N * 4), lane * 4);
             be = ld_f32(make_rsrc(beta + node0, N * 4), lane * 4);
         }
@@ -223,8 +232,8 @@ template <int NP, bool F32IN, bool FUSE, bool SBF>
 __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_kernel(
     const void *S0, const void *__restrict__ q_, const void *__restrict__ k_,
     const void *__restrict__ v_, const float *__restrict__ alpha, const float *__restrict__ beta,
-    const int32_t *__restrict__ parent, int N, int H, int units, void *__restrict__ o_,
-    float *U, int32_t *__restrict__ err, CommitArgs cm) {
+    const int32_t *__restrict__ parent, int N, int in_stride, int u_stride, int H, int units,
+    void *__restrict__ o_, float *U, int32_t *__restrict__ err, CommitArgs cm) {
     using In = typename std::conditional<F32IN, float, __bf16>::type;
     static_assert(!(SBF && F32IN), "a bf16 state is paired with bf16 inputs");
     using L = VerifyLds<NP, F32IN, FUSE>;
@@ -280,7 +289,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         const int par_a = __shfl(rd.cp_par, src);
         const float al_a = __shfl(rd.cp_al, src);
         bool bad = !len_ok;
-        if (lane < len) bad = bad || a < 0 || a >= cm.N_prev || a <= pa || (cm.parent && par_a != pa);
+        const bool check_parent = cm.parent || cm.chain_len >= 0;
+        if (lane < len) bad = bad || a < 0 || a >= cm.N_prev || a <= pa || (check_parent && par_a != pa);
         const bool ok = !__any(bad);
         const int len_c = ok ? len : 0;
         float x = lane < len_c ? al_a : 1.f;
@@ -315,7 +325,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         const int l32 = lane & 31, hg = lane >> 5;
         const int col = wave * 32 + l32;                 // this lane's d_v column (= row of S0)
         const int b = u / H;
-        const size_t node0 = (size_t)u * N;              // row of node 0 of this unit in q/k/v/o/U
+        const size_t node0 = (size_t)u * in_stride;      // row of node 0 of this unit in q/k/v/alpha/beta/o
+        const size_t unode0 = (size_t)u * u_stride;      // ... and in U
 
         // Fused commit, per thread: one k chunk (KCH elements of d_k) and one
         // U chunk (4 of d_v) of the CL path rows staged per pass.
@@ -323,9 +334,9 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         const int kl = tid / KCPR, kc = (tid % KCPR) * KCH;
         const int ul = tid / 32, uc = (tid % 32) * 4;
         constexpr int OOB = 1 << 30;                     // past every descriptor: reads zero
-        const rsrc_t rkp = make_rsrc(FUSE ? static_cast<const In *>(cm.k) + (size_t)u * cm.N_prev * D : nullptr,
+        const rsrc_t rkp = make_rsrc(FUSE ? static_cast<const In *>(cm.k) + (size_t)u * cm.in_stride * D : nullptr,
                                      FUSE ? cm.N_prev * D * (int)sizeof(In) : 0);
-        const rsrc_t rup = make_rsrc(FUSE ? cm.U + (size_t)u * cm.N_prev * D : nullptr,
+        const rsrc_t rup = make_rsrc(FUSE ? cm.U + (size_t)u * cm.u_stride * D : nullptr,
                                      FUSE ? cm.N_prev * D * 4 : 0);
         const int *c_node = meta_node(buf);
         const float *c_w = meta_w(buf);
@@ -363,7 +374,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             if (wave == 3 && has_next) rd.issue_path(cm, u_next, u_next / H, lane);
             stage_load(0, clen, cp_kv, cp_uv);
         }
-        rd.issue(S0, q, k, v, alpha, beta, parent, u, b, N, tid, lane, wave, hg, col);
+        rd.issue(S0, q, k, v, alpha, beta, parent, u, b, N, in_stride, tid, lane, wave, hg, col);
 
         // ---- phase 1: ancestors and cumulative decay by pointer jumping ----
         // Lane t of wave 0 keeps (ptr, prod, mask): ptr an ancestor of t (or
@@ -758,7 +769,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             __builtin_amdgcn_sched_barrier(0);
         }
         __syncthreads();                                 // every wave is done reading T
-        const rsrc_t ru = make_rsrc(U + node0 * D, N * D * 4);
+        const rsrc_t ru = make_rsrc(U + unode0 * D, N * D * 4);
         const rsrc_t ro = make_rsrc(o + node0 * D, N * D * (int)sizeof(In));
 #pragma unroll
         for (int m = 0; m < MT; ++m)
@@ -836,28 +847,27 @@ int resident_grid(int units) {
 
 template <int NP, bool F32IN, bool FUSE, bool SBF>
 hipError_t launch(const void *S0, const void *q, const void *k, const void *v, const float *alpha,
-                  const float *beta, const int32_t *parent, int N, int B, int H, void *o, float *U,
-                  int32_t *err, const CommitArgs &cm, hipStream_t stream) {
+                  const float *beta, const int32_t *parent, int N, int in_stride, int u_stride, int B, int H,
+                  void *o, float *U, int32_t *err, const CommitArgs &cm, hipStream_t stream) {
     const int units = B * H;
     hipLaunchKernelGGL((verify_kernel<NP, F32IN, FUSE, SBF>),
                        dim3((unsigned)resident_grid<NP, F32IN, FUSE, SBF>(units)), dim3(THREADS), 0, stream, S0, q,
-                       k, v, alpha, beta, parent, N, H, units, o, U, err, cm);
+                       k, v, alpha, beta, parent, N, in_stride, u_stride, H, units, o, U, err, cm);
     return hipGetLastError();
 }
 
 // fp32 inputs pair with an fp32 state (the caller checks); a bf16 state with bf16 inputs.
 template <bool FUSE>
 hipError_t dispatch(const void *S0, const void *q, const void *k, const void *v, const float *alpha,
-                    const float *beta, const int32_t *parent, int N, int B, int H, bool f32_in, bool bf16_state,
-                    void *o, float *U, int32_t *err, const CommitArgs &cm, hipStream_t stream) {
-    if (bf16_state)
-        return N <= 32 ? launch<32, false, FUSE, true>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream)
-                       : launch<64, false, FUSE, true>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream);
-    if (N <= 32)
-        return f32_in ? launch<32, true, FUSE, false>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream)
-                      : launch<32, false, FUSE, false>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream);
-    return f32_in ? launch<64, true, FUSE, false>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream)
-                  : launch<64, false, FUSE, false>(S0, q, k, v, alpha, beta, parent, N, B, H, o, U, err, cm, stream);
+                    const float *beta, const int32_t *parent, int N, int in_stride, int u_stride, int B, int H,
+                    bool f32_in, bool bf16_state, void *o, float *U, int32_t *err, const CommitArgs &cm,
+                    hipStream_t stream) {
+#define TREEWY_LAUNCH(NP, F, S)                                                                               \
+    launch<NP, F, FUSE, S>(S0, q, k, v, alpha, beta, parent, N, in_stride, u_stride, B, H, o, U, err, cm, stream)
+    if (bf16_state) return N <= 32 ? TREEWY_LAUNCH(32, false, true) : TREEWY_LAUNCH(64, false, true);
+    if (N <= 32) return f32_in ? TREEWY_LAUNCH(32, true, false) : TREEWY_LAUNCH(32, false, false);
+    return f32_in ? TREEWY_LAUNCH(64, true, false) : TREEWY_LAUNCH(64, false, false);
+#undef TREEWY_LAUNCH
 }
 
 }  // namespace
@@ -867,7 +877,8 @@ hipError_t launch_verify(const void *S0, const void *q, const void *k, const voi
                          int B, int H, bool f32_in, bool bf16_state, void *o, float *U, int32_t *err,
                          hipStream_t stream) {
     const CommitArgs none = {};
-    return dispatch<false>(S0, q, k, v, alpha, beta, parent, N, B, H, f32_in, bf16_state, o, U, err, none, stream);
+    return dispatch<false>(S0, q, k, v, alpha, beta, parent, N, N, N, B, H, f32_in, bf16_state, o, U, err, none,
+                           stream);
 }
 
 hipError_t launch_commit_verify(const void *S_old, const float *U_prev, const void *k_prev,
@@ -876,8 +887,25 @@ hipError_t launch_commit_verify(const void *S_old, const float *U_prev, const vo
                                 const void *k, const void *v, const float *alpha, const float *beta,
                                 const int32_t *parent, int N, int B, int H, bool f32_in, bool bf16_state,
                                 void *S_new, void *o, float *U, int32_t *err, hipStream_t stream) {
-    const CommitArgs cm = {U_prev, k_prev, alpha_prev, path, path_len, parent_prev, S_new, L_max, N_prev};
-    return dispatch<true>(S_old, q, k, v, alpha, beta, parent, N, B, H, f32_in, bf16_state, o, U, err, cm, stream);
+    const CommitArgs cm = {U_prev, k_prev, alpha_prev, path, path_len, parent_prev, S_new, L_max, N_prev,
+                           N_prev, N_prev, -1};
+    return dispatch<true>(S_old, q, k, v, alpha, beta, parent, N, N, N, B, H, f32_in, bf16_state, o, U, err, cm,
+                          stream);
+}
+
+// Chain prefill, one chunk of at most 64 tokens per launch (see treewy_chain_prefill).
+hipError_t launch_prefill_chunk(const void *S_old, const float *U_prev, const void *k_prev,
+                                const float *alpha_prev, int n_prev, const void *q, const void *k,
+                                const void *v, const float *alpha, const float *beta, int n, int T, int B,
+                                int H, bool f32_in, bool bf16_state, void *S_new, void *o, float *U,
+                                int32_t *err, hipStream_t stream) {
+    if (n_prev < 0)                                      // first chunk: plain verify from S0
+        return dispatch<false>(S_old, q, k, v, alpha, beta, nullptr, n, T, 64, B, H, f32_in, bf16_state, o, U,
+                               err, CommitArgs{}, stream);
+    const CommitArgs cm = {U_prev, k_prev, alpha_prev, nullptr, nullptr, nullptr, S_new, n_prev, n_prev, T, 64,
+                           n_prev};
+    return dispatch<true>(S_old, q, k, v, alpha, beta, nullptr, n, T, 64, B, H, f32_in, bf16_state, o, U, err, cm,
+                          stream);
 }
 
 }  // namespace treewy

@@ -26,7 +26,7 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     assert names == sorted(["treewy_verify", "treewy_commit", "treewy_commit_verify", "treewy_snapshot_verify",
                             "treewy_snapshot_commit", "treewy_path_from_node", "treewy_accept_greedy",
-                            "treewy_status_string"])
+                            "treewy_chain_prefill", "treewy_status_string"])
 
 
 def test_library_exports_every_declared_symbol(tw):
@@ -142,6 +142,24 @@ def test_accept_greedy_host_checks(tw):
     assert call(plen=None) == tw.TREEWY_ERR_INVALID_ARG
     assert call(path=None) == tw.TREEWY_ERR_INVALID_ARG
     assert call(B=0, root=None, plen=None) == tw.TREEWY_OK
+
+
+def test_chain_prefill_host_checks(tw):
+    f = tw.lib.treewy_chain_prefill
+
+    def call(S0=A, q=A, T=100, B=2, H=2, dk=128, dt=1, st=0, S_T=A, o=A, U=A):
+        return f(S0, q, A, A, A, A, T, B, H, dk, 128, dt, st, S_T, o, U, None, None)
+
+    assert call(T=-1) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(dk=64) == tw.TREEWY_ERR_UNSUPPORTED
+    assert call(dt=0, st=1) == tw.TREEWY_ERR_UNSUPPORTED
+    assert call(st=4) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(S0=None) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(U=None) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(q=M) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(T=1 << 29, B=4) == tw.TREEWY_ERR_UNSUPPORTED
+    assert call(B=0, S0=None) == tw.TREEWY_OK
+    assert call(T=0, S_T=A, S0=A) == tw.TREEWY_OK           # in place, nothing to copy
 
 
 def test_binding_raises_with_status(tw):
