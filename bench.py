@@ -338,18 +338,16 @@ def main():
         qp = wl.warmup_chunk_torch(w, args.seed, 2, Tp, "cuda", torch.bfloat16)[0]
         S_p = torch.empty_like(d["S0"])
         o_p = torch.empty_like(vp)
-        U_p = torch.empty((2, w.B, w.H, 64, w.d_v), dtype=torch.float32, device="cuda")
 
         def prefill():
-            tw.treewy_chain_prefill(d["S0"], qp, kp, vp, ap, bp, S_T=S_p, o=o_p, U_work=U_p)
+            tw.treewy_chain_prefill(d["S0"], qp, kp, vp, ap, bp, S_T=S_p, o=o_p)
 
         _, (ms_pf,) = time_steps(torch, [prefill], max(3, args.steps // 10), 1)
         pb = acc.prefill_bytes(w, Tp)
         result["chain_prefill"] = dict(roofline(pb, ms_pf, None), tokens=Tp,
-                                       tokens_per_s=round(w.B * Tp / (ms_pf * 1e-3), 1),
-                                       launches=(Tp + 63) // 64 + 1)
+                                       tokens_per_s=round(w.B * Tp / (ms_pf * 1e-3), 1))
         log("chain prefill of %d tokens: %.4f ms" % (Tp, ms_pf))
-        del kp, vp, ap, bp, qp, S_p, o_p, U_p
+        del kp, vp, ap, bp, qp, S_p, o_p
     # Greedy acceptance on the device (tokens: vocabulary of 4, the target
     # agreeing with the drafter along one planted chain per sequence).
     tok = wl.acceptance_tokens(x["parent"], seed=args.seed, vocab=4, plant=True)

@@ -149,26 +149,26 @@ treewy_status treewy_commit_verify(const void *S_old, const float *U_prev, const
 /*
  * treewy_chain_prefill - run the gated delta rule (Background, eq. 1) over a
  * chain of T tokens per unit and return every token's output and the final
- * state, in chunks of at most 64 tokens.  This is the chain WY form the tree
- * method generalises (Related work and Method: DeltaNet's chain transform):
- * each chunk is one chain verify (eq. 2) from the current state, and its
- * last token's state is rebuilt with eq. 3 and becomes the next chunk's S0
- * (the fused call, so the state is read once per chunk): ceil(T / 64) + 1 launches on
- * `stream`, the last one only commits.
+ * state.  This is the chain WY form that the tree method generalises
+ * (Related work and Method: DeltaNet's chain transform): in chunks of 64
+ * tokens, each chunk is one chain verify (eq. 2) from the current state, and
+ * the state after its last token is rebuilt with eq. 3 and becomes the next
+ * chunk's S0.  One launch on `stream`; the state stays on chip between
+ * chunks, so it is read and written once per unit.
  *   S0     [B, H, d_v, d_k] state_dtype   initial state (read only unless S_T == S0)
  *   q, k   [B, H, T, d_k]   in_dtype
  *   v      [B, H, T, d_v]   in_dtype
  *   alpha, beta [B, H, T]   float32
  *   S_T    [B, H, d_v, d_k] state_dtype   written: the state after token T - 1; may be S0
  *   o      [B, H, T, d_v]   in_dtype      written: o_t = S_t q_t for every token
- *   U_work [2, B, H, 64, d_v] float32     caller-owned workspace (pseudo-values of two chunks)
  *   err    [B] int32 or NULL
- * T >= 0 with T * B * H < 2^31; T == 0 copies S0 to S_T.
+ * T >= 0 with T * B * H < 2^31; T == 0 copies S0 to S_T.  A bf16 state is
+ * rounded once per chunk, as chunk-by-chunk commits would round it.
  */
 treewy_status treewy_chain_prefill(const void *S0, const void *q, const void *k, const void *v,
                                    const float *alpha, const float *beta, int T, int B, int H, int d_k, int d_v,
                                    treewy_dtype in_dtype, treewy_dtype state_dtype, void *S_T, void *o,
-                                   float *U_work, int32_t *err, void *stream);
+                                   int32_t *err, void *stream);
 
 /*
  * treewy_snapshot_verify - full-state-snapshotting baseline (Section "The

@@ -104,7 +104,7 @@ treewy_status treewy_commit_verify(const void *S_old, const float *U_prev, const
 treewy_status treewy_chain_prefill(const void *S0, const void *q, const void *k, const void *v,
                                    const float *alpha, const float *beta, int T, int B, int H, int d_k, int d_v,
                                    treewy_dtype in_dtype, treewy_dtype state_dtype, void *S_T, void *o,
-                                   float *U_work, int32_t *err, void *stream) {
+                                   int32_t *err, void *stream) {
     if (T < 0) return TREEWY_ERR_INVALID_ARG;
     treewy_status st = check_common(0, B, H, d_k, d_v, in_dtype);
     if (st == TREEWY_OK) st = check_state(state_dtype, in_dtype);
@@ -112,38 +112,16 @@ treewy_status treewy_chain_prefill(const void *S0, const void *q, const void *k,
     if ((int64_t)T * B * H > INT32_MAX) return TREEWY_ERR_UNSUPPORTED;
     if (B == 0 || H == 0) return TREEWY_OK;
     if (!S0 || !S_T) return TREEWY_ERR_INVALID_ARG;
-    if (T > 0 && (!q || !k || !v || !alpha || !beta || !o || !U_work)) return TREEWY_ERR_INVALID_ARG;
-    if (!aligned16(S0) || !aligned16(S_T) || !aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) ||
-        !aligned16(U_work))
+    if (T > 0 && (!q || !k || !v || !alpha || !beta || !o)) return TREEWY_ERR_INVALID_ARG;
+    if (!aligned16(S0) || !aligned16(S_T) || !aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
         return TREEWY_ERR_INVALID_ARG;
     const hipStream_t s = static_cast<hipStream_t>(stream);
-    const size_t state_bytes = (size_t)B * H * treewy::D * treewy::D * (state_dtype == TREEWY_BF16 ? 2 : 4);
-    if (T == 0)
-        return S_T == S0 ? TREEWY_OK : hip_status(hipMemcpyAsync(S_T, S0, state_bytes, hipMemcpyDeviceToDevice, s));
-    // Chunks of at most 64 tokens.  Chunk c is verified as a chain from the
-    // state after chunk c - 1, which the same launch first commits from chunk
-    // c - 1's pseudo-values (the fused call); a last launch with no tokens
-    // commits the final chunk.  Pseudo-values alternate between the two halves
-    // of U_work; the state lives in S_T from the second launch on.
-    const bool f32_in = in_dtype == TREEWY_F32, bf16_state = state_dtype == TREEWY_BF16;
-    const size_t esize = f32_in ? 4 : 2;
-    const size_t half = (size_t)B * H * 64 * treewy::D;
-    const char *qb = static_cast<const char *>(q), *kb = static_cast<const char *>(k);
-    const char *vb = static_cast<const char *>(v);
-    char *ob = static_cast<char *>(o);
-    const int chunks = (T + 63) / 64;
-    for (int c = 0; c <= chunks; ++c) {
-        const int t0 = 64 * c, n = c < chunks ? (T - t0 < 64 ? T - t0 : 64) : 0;
-        const int tp = 64 * (c - 1), n_prev = c == 0 ? -1 : (T - tp < 64 ? T - tp : 64);
-        const size_t row = (size_t)(c < chunks ? t0 : 0) * treewy::D * esize;
-        const size_t row_prev = (size_t)(c > 0 ? tp : 0) * treewy::D * esize;
-        hipError_t e = treewy::launch_prefill_chunk(
-            c <= 1 ? S0 : S_T, U_work + (size_t)((c + 1) & 1) * half, kb + row_prev, alpha + (c > 0 ? tp : 0), n_prev,
-            qb + row, kb + row, vb + row, alpha + (c < chunks ? t0 : 0), beta + (c < chunks ? t0 : 0), n, T, B, H,
-            f32_in, bf16_state, S_T, ob + row, U_work + (size_t)(c & 1) * half, err, s);
-        if (e != hipSuccess) return TREEWY_ERR_HIP;
+    if (T == 0) {
+        const size_t bytes = (size_t)B * H * treewy::D * treewy::D * (state_dtype == TREEWY_BF16 ? 2 : 4);
+        return S_T == S0 ? TREEWY_OK : hip_status(hipMemcpyAsync(S_T, S0, bytes, hipMemcpyDeviceToDevice, s));
     }
-    return TREEWY_OK;
+    return hip_status(treewy::launch_prefill(S0, q, k, v, alpha, beta, T, B, H, in_dtype == TREEWY_F32,
+                                             state_dtype == TREEWY_BF16, S_T, o, err, s));
 }
 
 treewy_status treewy_snapshot_verify(const float *S0, const void *q, const void *k, const void *v,

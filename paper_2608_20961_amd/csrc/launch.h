@@ -20,14 +20,11 @@ hipError_t launch_commit_verify(const void *S_old, const float *U_prev, const vo
                                 const int32_t *parent, int N, int B, int H, bool f32_in, bool bf16_state,
                                 void *S_new, void *o, float *U, int32_t *err, hipStream_t stream);
 
-// One chunk of the chain prefill: commit the previous chunk (n_prev tokens,
-// n_prev < 0 for none) into the state, then verify this chunk (n tokens) as
-// a chain.  Inputs are slices of [B, H, T, ...] tensors; U is [B, H, 64, d_v].
-hipError_t launch_prefill_chunk(const void *S_old, const float *U_prev, const void *k_prev,
-                                const float *alpha_prev, int n_prev, const void *q, const void *k,
-                                const void *v, const float *alpha, const float *beta, int n, int T, int B,
-                                int H, bool f32_in, bool bf16_state, void *S_new, void *o, float *U,
-                                int32_t *err, hipStream_t stream);
+// Chain prefill: T tokens per unit in chunks of 64, one launch, the state in
+// registers between chunks; inputs and o are [B, H, T, ...].
+hipError_t launch_prefill(const void *S0, const void *q, const void *k, const void *v, const float *alpha,
+                          const float *beta, int T, int B, int H, bool f32_in, bool bf16_state, void *S_T, void *o,
+                          int32_t *err, hipStream_t stream);
 
 hipError_t launch_commit(const void *S0, const float *U, const void *k, const float *alpha,
                          const int32_t *path, const int32_t *path_len, int L_max,

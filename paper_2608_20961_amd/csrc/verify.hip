@@ -156,9 +156,8 @@ struct UnitReads {
 
     __device__ __forceinline__ void issue(const void *S0, const In *q, const In *k, const In *vv,
                                           const float *alpha, const float *beta, const int32_t *parent,
-                                          int u, int b, int N, int in_stride, int tid, int lane, int wave,
-                                          int hg, int col) {
-        const size_t node0 = (size_t)u * in_stride;
+                                          int u, int b, int N, size_t node0, bool load_state, int tid,
+                                          int lane, int wave, int hg, int col) {
         if (wave == 0) {
             par = parent ? ld_i32(make_rsrc(parent + (size_t)b * N, N * 4), lane * 4) : lane - 1;
             al = ld_f32(make_rsrc(alpha + node0, N * 4), lane * 4);
@@ -175,6 +174,7 @@ struct UnitReads {
         const rsrc_t rv = make_rsrc(vv + node0 * D, N * ROW);
 #pragma unroll
         for (int i = 0; i < VQN; ++i) vq[i] = ld_u32x4<STREAM>(rv, (tid + THREADS * i) * 16);
+        if (!load_state) return;                        // (chain prefill: the state is already in registers)
         const rsrc_t rs = make_rsrc(static_cast<const char *>(S0) + (size_t)u * D * D * SB, D * D * SB);
         const int base = (col * D + 4 * hg) * SB;
 #pragma unroll
@@ -228,14 +228,18 @@ __device__ __forceinline__ void sweep_column(float (&r)[NP], const float *Bm, in
     }
 }
 
-template <int NP, bool F32IN, bool FUSE, bool SBF>
-__global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_kernel(
+// Two workgroups per CU where 256 registers per lane suffice.  The chain
+// prefill keeps the state in registers through the whole chunk, which needs
+// the full register file (one workgroup per CU); so do fp32 inputs at 64 nodes.
+template <int NP, bool F32IN, bool FUSE, bool SBF, bool PRE>
+__global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || PRE) ? 1 : 2) void verify_kernel(
     const void *S0, const void *__restrict__ q_, const void *__restrict__ k_,
     const void *__restrict__ v_, const float *__restrict__ alpha, const float *__restrict__ beta,
-    const int32_t *__restrict__ parent, int N, int in_stride, int u_stride, int H, int units,
+    const int32_t *__restrict__ parent, int N_all, int in_stride, int u_stride, int H, int units,
     void *__restrict__ o_, float *U, int32_t *__restrict__ err, CommitArgs cm) {
     using In = typename std::conditional<F32IN, float, __bf16>::type;
     static_assert(!(SBF && F32IN), "a bf16 state is paired with bf16 inputs");
+    static_assert(!(PRE && (FUSE || NP != 64)), "the chain prefill runs 64-token chunks, unfused");
     using L = VerifyLds<NP, F32IN, FUSE>;
     using Reads = UnitReads<NP, F32IN, FUSE, SBF>;
     constexpr int SB = Reads::SB;
@@ -325,7 +329,12 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         const int l32 = lane & 31, hg = lane >> 5;
         const int col = wave * 32 + l32;                 // this lane's d_v column (= row of S0)
         const int b = u / H;
-        const size_t node0 = (size_t)u * in_stride;      // row of node 0 of this unit in q/k/v/alpha/beta/o
+        // Chain prefill: the unit's tokens in chunks of 64, the state kept in
+        // registers from one chunk to the next.  Otherwise one pass.
+        const int chunks = PRE ? (N_all + 63) / 64 : 1;
+        for (int chunk = 0; chunk < chunks; ++chunk) {
+        const int N = PRE ? (N_all - 64 * chunk < 64 ? N_all - 64 * chunk : 64) : N_all;
+        const size_t node0 = (size_t)u * in_stride + 64 * chunk;   // row of node 0 in q/k/v/alpha/beta/o
         const size_t unode0 = (size_t)u * u_stride;      // ... and in U
 
         // Fused commit, per thread: one k chunk (KCH elements of d_k) and one
@@ -374,7 +383,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             if (wave == 3 && has_next) rd.issue_path(cm, u_next, u_next / H, lane);
             stage_load(0, clen, cp_kv, cp_uv);
         }
-        rd.issue(S0, q, k, v, alpha, beta, parent, u, b, N, in_stride, tid, lane, wave, hg, col);
+        rd.issue(S0, q, k, v, alpha, beta, parent, u, b, N, node0, chunk == 0, tid, lane, wave, hg, col);
 
         // ---- phase 1: ancestors and cumulative decay by pointer jumping ----
         // Lane t of wave 0 keeps (ptr, prod, mask): ptr an ancestor of t (or
@@ -769,19 +778,23 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             __builtin_amdgcn_sched_barrier(0);
         }
         __syncthreads();                                 // every wave is done reading T
-        const rsrc_t ru = make_rsrc(U + unode0 * D, N * D * 4);
+        const rsrc_t ru = make_rsrc(PRE ? nullptr : U + unode0 * D, PRE ? 0 : N * D * 4);
         const rsrc_t ro = make_rsrc(o + node0 * D, N * D * (int)sizeof(In));
+        if constexpr (!PRE) {                            // (the chain prefill keeps U in registers and K in LDS)
 #pragma unroll
-        for (int m = 0; m < MT; ++m)
+            for (int m = 0; m < MT; ++m)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) Us[(32 * m + acc_row(r, hg)) * US + col] = accv[m][r];
+                for (int r = 0; r < 16; ++r) Us[(32 * m + acc_row(r, hg)) * US + col] = accv[m][r];
+        }
         __syncthreads();
         // U leaves as whole rows, 16 bytes per lane (rows of padding nodes fall
         // past the end of the descriptor and are dropped) while A U runs.
+        if constexpr (!PRE) {
 #pragma unroll
-        for (int it = 0; it < NP * (D / 4) / THREADS; ++it) {
-            const int idx = tid + THREADS * it, t = idx / (D / 4), c = (idx % (D / 4)) * 4;
-            st_u32x4<STREAM>(ru, (t * D + c) * 4, *reinterpret_cast<const uint4 *>(Us + t * US + c));
+            for (int it = 0; it < NP * (D / 4) / THREADS; ++it) {
+                const int idx = tid + THREADS * it, t = idx / (D / 4), c = (idx % (D / 4)) * 4;
+                st_u32x4<STREAM>(ru, (t * D + c) * 4, *reinterpret_cast<const uint4 *>(Us + t * US + c));
+            }
         }
 #pragma unroll
         for (int s = 0; s < 2 * MT; ++s) {
@@ -821,13 +834,73 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 for (int r = 0; r < 16; ++r)
                     st_f32<STREAM>(ro, ((32 * m + acc_row(r, hg)) * D + col) * 4, accp[MT + m][r]);
         }
-        __syncthreads();                                 // LDS is rewritten by the next unit
+        if constexpr (PRE) {
+            // The chunk's state, eq. 3 over the whole chunk:
+            //   S <- g_N S + sum_l (g_N / g_l) U_l k_l^T,
+            // on the matrix cores as (K^T)(w U) over 32-row blocks of d_k.  The
+            // B operand comes straight from the U accumulators (contraction in
+            // their row order), the A operand from K still staged in LDS in
+            // the same order; the result rows are this lane's S entries.
+            const float gN = g_s[N - 1];
+            bf16x8 ubh[2 * MT], ubl[2 * MT];
+#pragma unroll
+            for (int s2 = 0; s2 < 2 * MT; ++s2) {
+                float wu[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int l = 32 * (s2 >> 1) + acc_row(8 * (s2 & 1) + e, hg);
+                    wu[e] = l < N ? accv[s2 >> 1][8 * (s2 & 1) + e] * (gN / g_s[l]) : 0.f;
+                }
+                split8(wu, ubh[s2], ubl[s2]);
+            }
+#pragma unroll
+            for (int jb = 0; jb < 4; ++jb) {
+                const int kpos = Reads::kperm(32 * jb + l32);
+                f32x16 d = {};
+#pragma unroll
+                for (int s2 = 0; s2 < 2 * MT; ++s2) {
+                    bf16x8 a, alo;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int l = 32 * (s2 >> 1) + acc_row(8 * (s2 & 1) + e, hg);
+                        a[e] = Xh[l * XS + kpos];
+                        if constexpr (F32IN) alo[e] = Xl[l * XS + kpos];
+                    }
+                    d = mma(a, ubh[s2], d);
+                    d = mma(a, ubl[s2], d);
+                    if constexpr (F32IN) d = mma(alo, ubh[s2], d);
+                }
+#pragma unroll
+                for (int r = 0; r < 16; r += 4) {
+                    const int s2 = 2 * jb + (r >> 3), h = (r >> 2) & 1;
+                    f32x4 x = rd.sget(s2, h);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) x[i] = fmaf(gN, x[i], d[r + i]);
+                    rd.sset(s2, h, x);
+                }
+            }
+        }
+        __syncthreads();                                 // LDS is rewritten by the next unit / chunk
+        }                                                // chunk
+        if constexpr (PRE) {                             // the state after the unit's last token
+            const rsrc_t rn = make_rsrc(static_cast<char *>(cm.S_new) + (size_t)u * D * D * SB, D * D * SB);
+            const int sbase = (col * D + 4 * hg) * SB;
+#pragma unroll
+            for (int s2 = 0; s2 < 8; ++s2)
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    if constexpr (SBF)
+                        st_u32x2<STREAM>(rn, sbase + 32 * s2 + 16 * h, rd.s0[s2][h]);
+                    else
+                        st_u32x4<STREAM>(rn, sbase + 64 * s2 + 32 * h, __builtin_bit_cast(uint4, rd.s0[s2][h]));
+                }
+        }
     }
 }
 
 namespace {
 
-template <int NP, bool F32IN, bool FUSE, bool SBF>
+template <int NP, bool F32IN, bool FUSE, bool SBF, bool PRE = false>
 int resident_grid(int units) {
     static int per_device[64] = {0};
     int dev = 0;
@@ -836,7 +909,7 @@ int resident_grid(int units) {
         int cus = 0, blocks = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
             cus = 256;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, verify_kernel<NP, F32IN, FUSE, SBF>, THREADS,
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, verify_kernel<NP, F32IN, FUSE, SBF, PRE>, THREADS,
                                                          0) != hipSuccess ||
             blocks <= 0)
             blocks = 1;
@@ -845,14 +918,14 @@ int resident_grid(int units) {
     return units < per_device[dev] ? units : per_device[dev];
 }
 
-template <int NP, bool F32IN, bool FUSE, bool SBF>
+template <int NP, bool F32IN, bool FUSE, bool SBF, bool PRE = false>
 hipError_t launch(const void *S0, const void *q, const void *k, const void *v, const float *alpha,
                   const float *beta, const int32_t *parent, int N, int in_stride, int u_stride, int B, int H,
                   void *o, float *U, int32_t *err, const CommitArgs &cm, hipStream_t stream) {
     const int units = B * H;
-    hipLaunchKernelGGL((verify_kernel<NP, F32IN, FUSE, SBF>),
-                       dim3((unsigned)resident_grid<NP, F32IN, FUSE, SBF>(units)), dim3(THREADS), 0, stream, S0, q,
-                       k, v, alpha, beta, parent, N, in_stride, u_stride, H, units, o, U, err, cm);
+    hipLaunchKernelGGL((verify_kernel<NP, F32IN, FUSE, SBF, PRE>),
+                       dim3((unsigned)resident_grid<NP, F32IN, FUSE, SBF, PRE>(units)), dim3(THREADS), 0, stream,
+                       S0, q, k, v, alpha, beta, parent, N, in_stride, u_stride, H, units, o, U, err, cm);
     return hipGetLastError();
 }
 
@@ -893,19 +966,21 @@ hipError_t launch_commit_verify(const void *S_old, const float *U_prev, const vo
                           stream);
 }
 
-// Chain prefill, one chunk of at most 64 tokens per launch (see treewy_chain_prefill).
-hipError_t launch_prefill_chunk(const void *S_old, const float *U_prev, const void *k_prev,
-                                const float *alpha_prev, int n_prev, const void *q, const void *k,
-                                const void *v, const float *alpha, const float *beta, int n, int T, int B,
-                                int H, bool f32_in, bool bf16_state, void *S_new, void *o, float *U,
-                                int32_t *err, hipStream_t stream) {
-    if (n_prev < 0)                                      // first chunk: plain verify from S0
-        return dispatch<false>(S_old, q, k, v, alpha, beta, nullptr, n, T, 64, B, H, f32_in, bf16_state, o, U,
-                               err, CommitArgs{}, stream);
-    const CommitArgs cm = {U_prev, k_prev, alpha_prev, nullptr, nullptr, nullptr, S_new, n_prev, n_prev, T, 64,
-                           n_prev};
-    return dispatch<true>(S_old, q, k, v, alpha, beta, nullptr, n, T, 64, B, H, f32_in, bf16_state, o, U, err, cm,
-                          stream);
+// Chain prefill: every chunk of every unit in one launch, the state kept in
+// registers between chunks (see treewy_chain_prefill).
+hipError_t launch_prefill(const void *S0, const void *q, const void *k, const void *v, const float *alpha,
+                          const float *beta, int T, int B, int H, bool f32_in, bool bf16_state, void *S_T, void *o,
+                          int32_t *err, hipStream_t stream) {
+    CommitArgs cm = {};
+    cm.S_new = S_T;
+    if (bf16_state)
+        return launch<64, false, false, true, true>(S0, q, k, v, alpha, beta, nullptr, T, T, 0, B, H, o, nullptr,
+                                                   err, cm, stream);
+    if (f32_in)
+        return launch<64, true, false, false, true>(S0, q, k, v, alpha, beta, nullptr, T, T, 0, B, H, o, nullptr,
+                                                   err, cm, stream);
+    return launch<64, false, false, false, true>(S0, q, k, v, alpha, beta, nullptr, T, T, 0, B, H, o, nullptr, err,
+                                                cm, stream);
 }
 
 }  // namespace treewy

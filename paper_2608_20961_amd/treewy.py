@@ -53,7 +53,7 @@ lib.treewy_path_from_node.argtypes = [_P, _P, _I, _I, _I, _P, _P, _P, _P]
 lib.treewy_path_from_node.restype = _I
 lib.treewy_accept_greedy.argtypes = [_P] * 4 + [_I] * 3 + [_P] * 5
 lib.treewy_accept_greedy.restype = _I
-lib.treewy_chain_prefill.argtypes = [_P] * 6 + [_I] * 7 + [_P] * 5
+lib.treewy_chain_prefill.argtypes = [_P] * 6 + [_I] * 7 + [_P] * 4
 lib.treewy_chain_prefill.restype = _I
 lib.treewy_status_string.argtypes = [_I]
 lib.treewy_status_string.restype = ctypes.c_char_p
@@ -271,10 +271,10 @@ def treewy_accept_greedy(parent, draft_token, target_token, root_token, L_max: i
     return path, path_len, bonus
 
 
-def treewy_chain_prefill(S0, q, k, v, alpha, beta, S_T=None, o=None, U_work=None, err=None, stream=None
+def treewy_chain_prefill(S0, q, k, v, alpha, beta, S_T=None, o=None, err=None, stream=None
                          ) -> Tuple[torch.Tensor, torch.Tensor]:
-    """Gated delta rule over a chain of T tokens per unit, in chunks of 64:
-    returns the final state and every token's output."""
+    """Gated delta rule over a chain of T tokens per unit (chunks of 64, one
+    launch): returns the final state and every token's output."""
     B, H, T, dk = q.shape
     dv = v.shape[-1]
     dt = q.dtype
@@ -285,13 +285,10 @@ def treewy_chain_prefill(S0, q, k, v, alpha, beta, S_T=None, o=None, U_work=None
         S_T = torch.empty_like(S0)
     if o is None:
         o = torch.empty((B, H, T, dv), dtype=dt, device=q.device)
-    if U_work is None:
-        U_work = torch.empty((2, B, H, 64, dv), dtype=torch.float32, device=q.device)
     _need(S_T, "S_T", S0.dtype, (B, H, dv, dk)); _need(o, "o", dt, (B, H, T, dv))
-    _need(U_work, "U_work", torch.float32, (2, B, H, 64, dv))
     if err is not None:
         _need(err, "err", torch.int32, (B,))
     _check(lib.treewy_chain_prefill(_ptr(S0), _ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(beta), T, B, H, dk, dv,
-                                    _in_dtype(q), _state_dtype(S0), _ptr(S_T), _ptr(o), _ptr(U_work), _ptr(err),
-                                    _stream(stream)), "treewy_chain_prefill")
+                                    _in_dtype(q), _state_dtype(S0), _ptr(S_T), _ptr(o), _ptr(err), _stream(stream)),
+           "treewy_chain_prefill")
     return S_T, o

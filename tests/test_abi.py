@@ -147,15 +147,15 @@ def test_accept_greedy_host_checks(tw):
 def test_chain_prefill_host_checks(tw):
     f = tw.lib.treewy_chain_prefill
 
-    def call(S0=A, q=A, T=100, B=2, H=2, dk=128, dt=1, st=0, S_T=A, o=A, U=A):
-        return f(S0, q, A, A, A, A, T, B, H, dk, 128, dt, st, S_T, o, U, None, None)
+    def call(S0=A, q=A, T=100, B=2, H=2, dk=128, dt=1, st=0, S_T=A, o=A):
+        return f(S0, q, A, A, A, A, T, B, H, dk, 128, dt, st, S_T, o, None, None)
 
     assert call(T=-1) == tw.TREEWY_ERR_INVALID_ARG
     assert call(dk=64) == tw.TREEWY_ERR_UNSUPPORTED
     assert call(dt=0, st=1) == tw.TREEWY_ERR_UNSUPPORTED
     assert call(st=4) == tw.TREEWY_ERR_INVALID_ARG
     assert call(S0=None) == tw.TREEWY_ERR_INVALID_ARG
-    assert call(U=None) == tw.TREEWY_ERR_INVALID_ARG
+    assert call(o=None) == tw.TREEWY_ERR_INVALID_ARG
     assert call(q=M) == tw.TREEWY_ERR_INVALID_ARG
     assert call(T=1 << 29, B=4) == tw.TREEWY_ERR_UNSUPPORTED
     assert call(B=0, S0=None) == tw.TREEWY_OK
