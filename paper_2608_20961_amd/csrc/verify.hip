@@ -383,7 +383,9 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || PRE) ? 1 : 2) void
             if (wave == 3 && has_next) rd.issue_path(cm, u_next, u_next / H, lane);
             stage_load(0, clen, cp_kv, cp_uv);
         }
-        rd.issue(S0, q, k, v, alpha, beta, parent, u, b, N, node0, chunk == 0, tid, lane, wave, hg, col);
+        constexpr bool AHEAD = PRE && !F32IN;            // prefill fetches the next chunk early (bf16 inputs)
+        if (!AHEAD || chunk == 0)                        // (then later chunks were fetched one chunk ahead)
+            rd.issue(S0, q, k, v, alpha, beta, parent, u, b, N, node0, chunk == 0, tid, lane, wave, hg, col);
 
         // ---- phase 1: ancestors and cumulative decay by pointer jumping ----
         // Lane t of wave 0 keeps (ptr, prod, mask): ptr an ancestor of t (or
@@ -471,6 +473,15 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || PRE) ? 1 : 2) void
                 }
         }
         __syncthreads();
+        // Chain prefill: this chunk's reads are in LDS and registers now, so the
+        // next chunk's are issued into the same registers and land during this
+        // chunk's arithmetic (fp32 inputs need twice the registers: not there).
+        if constexpr (AHEAD) {
+            if (chunk + 1 < chunks) {
+                const int N1 = N_all - 64 * (chunk + 1) < 64 ? N_all - 64 * (chunk + 1) : 64;
+                rd.issue(S0, q, k, v, alpha, beta, parent, u, b, N1, node0 + 64, false, tid, lane, wave, hg, col);
+            }
+        }
 
         // ---- phase 2: masked, decay-weighted gram tiles (lower triangle) --
         //   B[t,i] = beta_t (g_t/g_i) (k_t . k_i)  for i a strict ancestor of t
@@ -644,24 +655,61 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || PRE) ? 1 : 2) void
         // column i (from the last down) T[t, i] = -r[i] is final and row i
         // of B (one broadcast read) is added in.  B is zero off the ancestor
         // pattern, so the sweep reaches the same T for any tree; it costs
-        // NP^2 / 2 fused multiply-adds per lane and no dependent LDS reads.
-        // Every read of B precedes the final row stores.
+        // n^2 / 2 fused multiply-adds per lane and no dependent LDS reads.
+        // Every read of B precedes the final row stores.  With 64 rows, T is
+        // built in 32 x 32 blocks on the same wave: both diagonal blocks
+        // (T00 = inverse of I + B00 on lanes 0-31, T11 = inverse of I + B11
+        // on lanes 32-63) in one sweep, then T10 = -T11 (B10 T00) on the
+        // matrix cores, in place over B10 (M = B10 T00 is parked there first
+        // so that one accumulator tile is live at a time).  LDS accesses of
+        // one wave complete in order, so no barrier separates the steps.
         if (!shallow && wave == 3) {
-            const int t = lane < NP ? lane : NP - 1;
-            float r[NP];
+            const int tl = lane & 31;                                // row within a diagonal block
+            const int off = NP == 64 ? 32 * (lane >> 5) : 0;
+            const float *Bblk = Bm + off * MS + off;
+            float r[32];
 #pragma unroll
-            for (int c = 0; c < NP / 4; ++c) {
-                const f32x4 bt = *reinterpret_cast<const f32x4 *>(Bm + t * MS + 4 * c);
+            for (int c = 0; c < 8; ++c) {
+                const f32x4 bt = *reinterpret_cast<const f32x4 *>(Bblk + tl * MS + 4 * c);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) r[4 * c + e] = bt[e];
             }
-            sweep_column<NP - 1, NP, MS>(r, Bm, t, 0.f);
-            if (lane < NP) {
-                float *Tt = Bm + t * MS;
+            sweep_column<31, 32, MS>(r, Bblk, tl, 0.f);
+            if (NP == 64 || lane < 32) {
+                float *Tt = Bm + (off + tl) * MS + off;
 #pragma unroll
-                for (int c = 0; c < NP / 4; ++c)
+                for (int c = 0; c < 8; ++c)
                     *reinterpret_cast<f32x4 *>(Tt + 4 * c) = f32x4{r[4 * c], r[4 * c + 1], r[4 * c + 2], r[4 * c + 3]};
-                if (t < N) Tt[t] = 1.f;
+                if (off + tl < N) Tt[tl] = 1.f;
+            }
+            if constexpr (NP == 64) {
+                // rows of the left factor and columns of the right one, 16 deep per step
+                auto block_product = [&](const float *Arow, const float *Bcol) {
+                    f32x16 acc = {};
+#pragma unroll
+                    for (int s2 = 0; s2 < 2; ++s2) {
+                        float a8[8], b8[8];
+                        *reinterpret_cast<f32x4 *>(a8) = *reinterpret_cast<const f32x4 *>(Arow + 16 * s2 + 8 * hg);
+                        *reinterpret_cast<f32x4 *>(a8 + 4) =
+                            *reinterpret_cast<const f32x4 *>(Arow + 16 * s2 + 8 * hg + 4);
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) b8[e] = Bcol[(16 * s2 + 8 * hg + e) * MS];
+                        bf16x8 ah, alo, bh, bl;
+                        split8(a8, ah, alo);
+                        split8(b8, bh, bl);
+                        acc = mma(ah, bh, acc);
+                        acc = mma(ah, bl, acc);
+                        acc = mma(alo, bh, acc);
+                    }
+                    return acc;
+                };
+                float *B10 = Bm + 32 * MS;
+                const f32x16 mm = block_product(B10 + l32 * MS, Bm + l32);            // B10 T00
+#pragma unroll
+                for (int r = 0; r < 16; ++r) B10[acc_row(r, hg) * MS + l32] = mm[r];
+                const f32x16 tt = block_product(B10 + l32 * MS + 32, B10 + l32);       // T11 M
+#pragma unroll
+                for (int r = 0; r < 16; ++r) B10[acc_row(r, hg) * MS + l32] = -tt[r];
             }
         }
 
