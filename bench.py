@@ -344,7 +344,7 @@ def main():
 
         _, (ms_pf,) = time_steps(torch, [prefill], max(3, args.steps // 10), 1)
         pb = acc.prefill_bytes(w, Tp)
-        result["chain_prefill"] = dict(roofline(pb, ms_pf, None), tokens=Tp,
+        result["chain_prefill"] = dict(roofline(pb, ms_pf, load_traffic("chain_prefill", w.name, src_hash)), tokens=Tp,
                                        tokens_per_s=round(w.B * Tp / (ms_pf * 1e-3), 1))
         log("chain prefill of %d tokens: %.4f ms" % (Tp, ms_pf))
         del kp, vp, ap, bp, qp, S_p, o_p
