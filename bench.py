@@ -49,6 +49,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--prefill-tokens", type=int, default=1024,
                    help="tokens per sequence for the chain-prefill measurement (0 skips it)")
+    p.add_argument("--no-big-tree", action="store_true", help="skip the 128-node tree (chunked verify)")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time for the CPU baseline")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain 1 GiB device copy (for scaling HBM counters)")
@@ -348,6 +349,39 @@ def main():
                                        tokens_per_s=round(w.B * Tp / (ms_pf * 1e-3), 1))
         log("chain prefill of %d tokens: %.4f ms" % (Tp, ms_pf))
         del kp, vp, ap, bp, qp, S_p, o_p
+    # Trees past one 64-node chunk: 128-node trees at the same layer shape
+    # (verify walks two chunks per unit; commit follows paths up to 16 long).
+    if not args.no_big_tree and w.in_dtype == "bf16" and w.B == wl.BIG_TREE.B and w.H == wl.BIG_TREE.H:
+        wb = wl.BIG_TREE
+        xb = wl.make_inputs(wb, seed=args.seed)
+        put = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to("cuda").to(dt)
+        bq, bk, bv = (put(xb[n], torch.bfloat16) for n in ("q", "k", "v"))
+        ba, bb = put(xb["alpha"], torch.float32), put(xb["beta"], torch.float32)
+        bpar, bpath, bplen = (put(xb[n], torch.int32) for n in ("parent", "path", "path_len"))
+        o_b = torch.empty((wb.B, wb.H, wb.N, wb.d_v), dtype=torch.bfloat16, device="cuda")
+        U_b = torch.empty((wb.B, wb.H, wb.N, wb.d_v), dtype=torch.float32, device="cuda")
+        S_nb = torch.empty_like(d["S0"])
+
+        def verify_big():
+            tw.treewy_verify(d["S0"], bq, bk, bv, ba, bb, bpar, o=o_b, U=U_b)
+
+        def commit_big():
+            tw.treewy_commit(S0_commit, U_b, bk, ba, bpath, bplen, parent=bpar, S_new=S_nb)
+
+        ms_bstep, (ms_bv, ms_bc) = time_steps(torch, [verify_big, commit_big], max(5, args.steps // 2),
+                                              max(2, args.warmup // 2))
+        nb = wb.B * wb.N
+        result["tree128"] = {
+            "workload": wb.describe(),
+            "ms_per_step": round(ms_bstep, 5),
+            "nodes_per_s": round(nb / (ms_bstep * 1e-3), 1),
+            "verify": dict(roofline(acc.verify_bytes(wb), ms_bv, load_traffic("verify", wb.name, src_hash)),
+                           nodes_per_s=round(nb / (ms_bv * 1e-3), 1)),
+            "commit": roofline(acc.commit_bytes(wb, xb["path_len"]), ms_bc,
+                               load_traffic("commit", wb.name, src_hash)),
+        }
+        log("128-node trees: verify %.4f ms, commit %.4f ms" % (ms_bv, ms_bc))
+        del bq, bk, bv, ba, bb, bpar, bpath, bplen, o_b, U_b, S_nb
     # Greedy acceptance on the device (tokens: vocabulary of 4, the target
     # agreeing with the drafter along one planted chain per sequence).
     tok = wl.acceptance_tokens(x["parent"], seed=args.seed, vocab=4, plant=True)

@@ -17,8 +17,9 @@
  *    whose base address is 16-byte aligned.  The caller allocates and owns
  *    every buffer; the library allocates nothing and keeps no state between
  *    calls, so calls are re-entrant.
- *  - Sizes supported: d_k == d_v == 128, 0 <= N <= 64 (N = 0 is an empty
- *    draft), 0 <= L_max <= 64, B * H < 2^31; other sizes return
+ *  - Sizes supported: d_k == d_v == 128, 0 <= N <= 256 (N = 0 is an empty
+ *    draft), 0 <= L_max <= 256, B * H < 2^31; the fused call and the
+ *    snapshot baseline take N, N_prev, L_max <= 64.  Other sizes return
  *    TREEWY_ERR_UNSUPPORTED, negative sizes TREEWY_ERR_INVALID_ARG.  B == 0 or
  *    H == 0 launches nothing and returns TREEWY_OK; so does N == 0 for the
  *    verify calls (commit with N == 0 still copies S0 to S_new).
@@ -45,7 +46,7 @@ extern "C" {
 typedef enum treewy_status {
     TREEWY_OK = 0,
     TREEWY_ERR_INVALID_ARG = 1,  /* null or misaligned pointer, negative size, bad dtype */
-    TREEWY_ERR_UNSUPPORTED = 2,  /* d_k or d_v != 128, N or L_max above 64, too many units */
+    TREEWY_ERR_UNSUPPORTED = 2,  /* d_k or d_v != 128, N or L_max too large, too many units */
     TREEWY_ERR_HIP = 3           /* the HIP runtime refused the launch */
 } treewy_status;
 
@@ -82,6 +83,13 @@ typedef enum treewy_dtype {
  *   o      [B, H, N, d_v]   in_dtype       written: every node's output
  *   U      [B, H, N, d_v]   float32        written: pseudo-values, read by treewy_commit
  *   err    [B] int32 or NULL               TREEWY_FLAG_BAD_PARENT
+ *
+ * Up to 64 nodes a unit is one pass.  Larger trees (65 to 256 nodes) are
+ * walked in chunks of 64 nodes in index order; the system is block lower
+ * triangular, so each chunk first adds the terms of its ancestors in earlier
+ * chunks (G and the output weights against the U rows already written for
+ * them) and then solves its own diagonal block.  The result is the same
+ * system solved whole.
  */
 treewy_status treewy_verify(const void *S0, const void *q, const void *k, const void *v,
                             const float *alpha, const float *beta, const int32_t *parent, int N,

@@ -7,7 +7,8 @@
 
 namespace {
 
-constexpr int kMaxN = 64;
+constexpr int kMaxTree = treewy::MAX_TREE;   // verify, commit and the tree helpers
+constexpr int kMaxOnePass = 64;              // the fused call and the snapshot baseline
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -21,11 +22,11 @@ treewy_status check_state(treewy_dtype state, treewy_dtype in) {
     return TREEWY_OK;
 }
 
-treewy_status check_common(int N, int B, int H, int d_k, int d_v, treewy_dtype dt) {
+treewy_status check_common(int N, int B, int H, int d_k, int d_v, treewy_dtype dt, int max_n) {
     if (B < 0 || H < 0 || N < 0) return TREEWY_ERR_INVALID_ARG;
     if (dt != TREEWY_F32 && dt != TREEWY_BF16) return TREEWY_ERR_INVALID_ARG;
     if (d_k != treewy::D || d_v != treewy::D) return TREEWY_ERR_UNSUPPORTED;
-    if (N > kMaxN) return TREEWY_ERR_UNSUPPORTED;
+    if (N > max_n) return TREEWY_ERR_UNSUPPORTED;
     if ((int64_t)B * H > INT32_MAX) return TREEWY_ERR_UNSUPPORTED;
     return TREEWY_OK;
 }
@@ -38,7 +39,7 @@ treewy_status treewy_verify(const void *S0, const void *q, const void *k, const 
                             const float *alpha, const float *beta, const int32_t *parent, int N,
                             int B, int H, int d_k, int d_v, treewy_dtype in_dtype, treewy_dtype state_dtype,
                             void *o, float *U, int32_t *err, void *stream) {
-    treewy_status st = check_common(N, B, H, d_k, d_v, in_dtype);
+    treewy_status st = check_common(N, B, H, d_k, d_v, in_dtype, kMaxTree);
     if (st == TREEWY_OK) st = check_state(state_dtype, in_dtype);
     if (st != TREEWY_OK) return st;
     if (N == 0 || B == 0 || H == 0) return TREEWY_OK;
@@ -56,11 +57,11 @@ treewy_status treewy_commit(const void *S0, const float *U, const void *k, const
                             const int32_t *parent, int N, int B, int H, int d_k, int d_v,
                             treewy_dtype k_dtype, treewy_dtype state_dtype, void *S_new, int32_t *err,
                             void *stream) {
-    treewy_status st = check_common(N, B, H, d_k, d_v, k_dtype);
+    treewy_status st = check_common(N, B, H, d_k, d_v, k_dtype, kMaxTree);
     if (st == TREEWY_OK && state_dtype != TREEWY_F32 && state_dtype != TREEWY_BF16) st = TREEWY_ERR_INVALID_ARG;
     if (st != TREEWY_OK) return st;
     if (L_max < 0) return TREEWY_ERR_INVALID_ARG;
-    if (L_max > kMaxN) return TREEWY_ERR_UNSUPPORTED;
+    if (L_max > kMaxTree) return TREEWY_ERR_UNSUPPORTED;
     if (B == 0 || H == 0) return TREEWY_OK;
     if (!S0 || !path_len || !S_new) return TREEWY_ERR_INVALID_ARG;
     if (N > 0 && (!U || !k || !alpha)) return TREEWY_ERR_INVALID_ARG;
@@ -79,11 +80,11 @@ treewy_status treewy_commit_verify(const void *S_old, const float *U_prev, const
                                    int N, int B, int H, int d_k, int d_v, treewy_dtype in_dtype,
                                    treewy_dtype state_dtype, void *S_new, void *o, float *U, int32_t *err,
                                    void *stream) {
-    treewy_status st = check_common(N, B, H, d_k, d_v, in_dtype);
+    treewy_status st = check_common(N, B, H, d_k, d_v, in_dtype, kMaxOnePass);
     if (st == TREEWY_OK) st = check_state(state_dtype, in_dtype);
     if (st != TREEWY_OK) return st;
     if (N_prev < 0 || L_max < 0) return TREEWY_ERR_INVALID_ARG;
-    if (N_prev > kMaxN || L_max > kMaxN) return TREEWY_ERR_UNSUPPORTED;
+    if (N_prev > kMaxOnePass || L_max > kMaxOnePass) return TREEWY_ERR_UNSUPPORTED;
     if (B == 0 || H == 0) return TREEWY_OK;
     if (!S_old || !path_len || !S_new) return TREEWY_ERR_INVALID_ARG;
     if (N_prev > 0 && (!U_prev || !k_prev || !alpha_prev)) return TREEWY_ERR_INVALID_ARG;
@@ -106,7 +107,7 @@ treewy_status treewy_chain_prefill(const void *S0, const void *q, const void *k,
                                    treewy_dtype in_dtype, treewy_dtype state_dtype, void *S_T, void *o,
                                    int32_t *err, void *stream) {
     if (T < 0) return TREEWY_ERR_INVALID_ARG;
-    treewy_status st = check_common(0, B, H, d_k, d_v, in_dtype);
+    treewy_status st = check_common(0, B, H, d_k, d_v, in_dtype, kMaxTree);
     if (st == TREEWY_OK) st = check_state(state_dtype, in_dtype);
     if (st != TREEWY_OK) return st;
     if ((int64_t)T * B * H > INT32_MAX) return TREEWY_ERR_UNSUPPORTED;
@@ -128,7 +129,7 @@ treewy_status treewy_snapshot_verify(const float *S0, const void *q, const void 
                                      const float *alpha, const float *beta, const int32_t *parent,
                                      int N, int B, int H, int d_k, int d_v, treewy_dtype in_dtype,
                                      void *o, float *snapshots, int32_t *err, void *stream) {
-    treewy_status st = check_common(N, B, H, d_k, d_v, in_dtype);
+    treewy_status st = check_common(N, B, H, d_k, d_v, in_dtype, kMaxOnePass);
     if (st != TREEWY_OK) return st;
     if (N == 0 || B == 0 || H == 0) return TREEWY_OK;
     if (!S0 || !q || !k || !v || !alpha || !beta || !parent || !o || !snapshots)
@@ -142,7 +143,7 @@ treewy_status treewy_snapshot_verify(const float *S0, const void *q, const void 
 treewy_status treewy_snapshot_commit(const float *S0, const float *snapshots, const int32_t *accepted,
                                      int N, int B, int H, int d_k, int d_v, float *S_new,
                                      int32_t *err, void *stream) {
-    treewy_status st = check_common(N, B, H, d_k, d_v, TREEWY_F32);
+    treewy_status st = check_common(N, B, H, d_k, d_v, TREEWY_F32, kMaxOnePass);
     if (st != TREEWY_OK) return st;
     if (B == 0 || H == 0) return TREEWY_OK;
     if (!S0 || !accepted || !S_new || (N > 0 && !snapshots)) return TREEWY_ERR_INVALID_ARG;
@@ -156,7 +157,7 @@ treewy_status treewy_path_from_node(const int32_t *parent, const int32_t *accept
                                     int L_max, int32_t *path, int32_t *path_len, int32_t *err,
                                     void *stream) {
     if (N < 0 || B < 0 || L_max < 0) return TREEWY_ERR_INVALID_ARG;
-    if (N > kMaxN || L_max > kMaxN) return TREEWY_ERR_UNSUPPORTED;
+    if (N > kMaxTree || L_max > kMaxTree) return TREEWY_ERR_UNSUPPORTED;
     if (B == 0) return TREEWY_OK;
     if (!accepted || !path_len || (N > 0 && !parent) || (L_max > 0 && !path))
         return TREEWY_ERR_INVALID_ARG;
@@ -169,7 +170,7 @@ treewy_status treewy_accept_greedy(const int32_t *parent, const int32_t *draft_t
                                    int L_max, int32_t *path, int32_t *path_len, int32_t *bonus,
                                    int32_t *err, void *stream) {
     if (N < 0 || B < 0 || L_max < 0) return TREEWY_ERR_INVALID_ARG;
-    if (N > kMaxN || L_max > kMaxN) return TREEWY_ERR_UNSUPPORTED;
+    if (N > kMaxTree || L_max > kMaxTree) return TREEWY_ERR_UNSUPPORTED;
     if (B == 0) return TREEWY_OK;
     if (!root_token || !path_len || (N > 0 && (!parent || !draft_token || !target_token)) ||
         (L_max > 0 && !path))
@@ -183,7 +184,9 @@ const char *treewy_status_string(treewy_status status) {
     switch (status) {
     case TREEWY_OK: return "ok";
     case TREEWY_ERR_INVALID_ARG: return "invalid argument (null or misaligned pointer, bad size or dtype)";
-    case TREEWY_ERR_UNSUPPORTED: return "unsupported size (d_k, d_v must be 128; N, L_max at most 64)";
+    case TREEWY_ERR_UNSUPPORTED:
+        return "unsupported size or dtype (d_k, d_v must be 128; N, L_max at most 256, and 64 for the fused call "
+               "and the snapshot baseline; a bf16 state needs bf16 inputs)";
     case TREEWY_ERR_HIP: return "HIP launch failed";
     }
     return "unknown status";

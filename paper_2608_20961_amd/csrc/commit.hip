@@ -8,15 +8,17 @@
 // bf16 state: 8 entries, read and written in eight chunks), so each load and
 // store instruction of the workgroup covers 4 KiB of contiguous HBM.  A bf16
 // state is updated in fp32 and rounded to nearest even on the way out.  The
-// path's scaled pseudo-value rows and keys (at most 64 x 128 each) are staged
-// in LDS.  Each thread reads and writes only its own elements, so S_new may
-// alias S0.
+// path is checked one entry per thread, its weights are suffix products
+// across one wave, and its scaled pseudo-value rows and keys are staged in
+// LDS 64 rows at a time.  Each thread reads and writes only its own
+// elements, so S_new may alias S0.
 #include "device.h"
 #include "launch.h"
 
 namespace treewy {
 
-constexpr int MAX_PATH = 64;
+constexpr int MAX_PATH = MAX_TREE;
+constexpr int STAGE_ROWS = 64;                           // path rows staged per pass
 
 template <bool F32K, bool SBF>
 __global__ __launch_bounds__(THREADS) void commit_kernel(
@@ -28,11 +30,12 @@ __global__ __launch_bounds__(THREADS) void commit_kernel(
     constexpr int CH = 16 / SB;                          // entries per 16-byte chunk
     constexpr int NCH = D * D / CH / THREADS;            // chunks per thread
     using In = typename std::conditional<F32K, float, __bf16>::type;
-    extern __shared__ __attribute__((aligned(16))) float stage[];   // Uw [L_max][D], Kp [L_max][D]
+    extern __shared__ __attribute__((aligned(16))) float stage[];   // Uw [cap][D], Kp [cap][D]
     __shared__ int s_node[MAX_PATH];
+    __shared__ float s_al[MAX_PATH];
     __shared__ float s_w[MAX_PATH];
     __shared__ float s_w0;
-    __shared__ int s_len;
+    __shared__ int s_bad;
 
     const In *k = static_cast<const In *>(k_);
     const int tid = threadIdx.x, u = blockIdx.x, b = u / H;
@@ -44,39 +47,55 @@ __global__ __launch_bounds__(THREADS) void commit_kernel(
 #pragma unroll
     for (int i = 0; i < NCH; ++i) raw[i] = ld_u32x4<STREAM>(rs, (tid + THREADS * i) * 16);
 
-    if (tid == 0) {
-        const int len = path_len[b];
-        bool ok = len >= 0 && len <= L_max;
-        int prev = -1;
-        for (int l = 0; ok && l < len; ++l) {
+    // Entry l is valid when it lies in [0, N), follows entry l - 1 in index
+    // order and (with a parent array) is its child, entry 0 a child of the
+    // committed prefix.  A bad path commits nothing.
+    const int len_in = path_len[b];
+    const bool len_ok = len_in >= 0 && len_in <= L_max;
+    if (tid == 0) s_bad = len_ok ? 0 : 1;
+    __syncthreads();
+    if (len_ok)
+        for (int l = tid; l < len_in; l += THREADS) {
             const int a = path[(size_t)b * L_max + l];
-            if (a < 0 || a >= N || a <= prev || (parent && parent[(size_t)b * N + a] != prev))
-                ok = false;
-            else
+            const int prev = l > 0 ? path[(size_t)b * L_max + l - 1] : -1;
+            if (a < 0 || a >= N || a <= prev || (parent && parent[(size_t)b * N + a] != prev)) {
+                s_bad = 1;
+            } else {
                 s_node[l] = a;
-            prev = a;
-        }
-        float w = 1.f;
-        if (ok)
-            for (int l = len - 1; l >= 0; --l) {
-                s_w[l] = w;
-                w *= alpha[node0 + s_node[l]];
+                s_al[l] = alpha[node0 + a];
             }
-        s_len = ok ? len : 0;
-        s_w0 = ok ? w : 1.f;
-        if (!ok) flag_error(err, b, TREEWY_FLAG_BAD_PATH);
+        }
+    __syncthreads();
+    const bool ok = s_bad == 0;
+    const int len = ok ? len_in : 0;
+    // w_l = product of alpha over the entries after l, and g_a = the product
+    // over all: lane i of wave 0 holds entries 4i .. 4i + 3.
+    if (tid < 64) {
+        float a4[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) a4[e] = 4 * tid + e < len ? s_al[4 * tid + e] : 1.f;
+        float x = a4[0] * a4[1] * a4[2] * a4[3];
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {         // x = product over lanes >= tid
+            const float y = __shfl_down(x, off);
+            x *= tid + off < 64 ? y : 1.f;
+        }
+        const float y = __shfl_down(x, 1);
+        float after = tid < 63 ? y : 1.f;                // product over the entries past this lane's four
+#pragma unroll
+        for (int e = 3; e >= 0; --e) {
+            if (4 * tid + e < len) s_w[4 * tid + e] = after;
+            after *= a4[e];
+        }
+        if (tid == 0) {
+            s_w0 = x;
+            if (!ok) flag_error(err, b, TREEWY_FLAG_BAD_PATH);
+        }
     }
     __syncthreads();
-    const int len = s_len;
+    const int cap = L_max < STAGE_ROWS ? L_max : STAGE_ROWS;
     float *Uw = stage;
-    float *Kp = stage + (size_t)L_max * D;
-    for (int idx = tid; idx < len * D; idx += THREADS) {
-        const int l = idx / D, c = idx % D;
-        const size_t row = (node0 + s_node[l]) * D + c;
-        Uw[idx] = s_w[l] * U[row];
-        Kp[idx] = to_f32(k[row]);
-    }
-    __syncthreads();
+    float *Kp = stage + (size_t)cap * D;
 
     // Chunk i of this thread holds row r0 + (THREADS / (D / CH)) i, entries [c0, c0 + CH).
     const float w0 = s_w0;
@@ -95,16 +114,28 @@ __global__ __launch_bounds__(THREADS) void commit_kernel(
             for (int e = 0; e < CH; ++e) x[i][e] = w0 * f[e];
         }
     }
-    for (int l = 0; l < len; ++l) {
-        float kk[CH];
+    for (int l0 = 0; l0 < len; l0 += cap) {             // uniform loop
+        const int n = len - l0 < cap ? len - l0 : cap;
+        if (l0 > 0) __syncthreads();                     // the previous pass is done with the stage
+        for (int idx = tid; idx < n * D; idx += THREADS) {
+            const int l = idx / D, c = idx % D;
+            const size_t row = (node0 + s_node[l0 + l]) * D + c;
+            Uw[idx] = s_w[l0 + l] * U[row];
+            Kp[idx] = to_f32(k[row]);
+        }
+        __syncthreads();
+        for (int l = 0; l < n; ++l) {
+            float kk[CH];
 #pragma unroll
-        for (int e = 0; e < CH; e += 4) *reinterpret_cast<f32x4 *>(kk + e) = *reinterpret_cast<const f32x4 *>(Kp + l * D + c0 + e);
-        const float *uw = Uw + l * D + r0;
+            for (int e = 0; e < CH; e += 4)
+                *reinterpret_cast<f32x4 *>(kk + e) = *reinterpret_cast<const f32x4 *>(Kp + l * D + c0 + e);
+            const float *uw = Uw + l * D + r0;
 #pragma unroll
-        for (int i = 0; i < NCH; ++i) {
-            const float a = uw[RSTEP * i];
+            for (int i = 0; i < NCH; ++i) {
+                const float a = uw[RSTEP * i];
 #pragma unroll
-            for (int e = 0; e < CH; ++e) x[i][e] += a * kk[e];
+                for (int e = 0; e < CH; ++e) x[i][e] += a * kk[e];
+            }
         }
     }
     const rsrc_t rd = make_rsrc(static_cast<char *>(S_new) + (size_t)u * D * D * SB, D * D * SB);
@@ -128,7 +159,7 @@ hipError_t launch_commit(const void *S0, const float *U, const void *k, const fl
                          const int32_t *parent, int N, int B, int H, bool f32_k, bool bf16_state,
                          void *S_new, int32_t *err, hipStream_t stream) {
     const dim3 grid((unsigned)(B * H)), block(THREADS);
-    const size_t lds = (size_t)2 * L_max * D * sizeof(float);
+    const size_t lds = (size_t)2 * (L_max < STAGE_ROWS ? L_max : STAGE_ROWS) * D * sizeof(float);
 #define TREEWY_COMMIT(F, S)                                                                                   \
     hipLaunchKernelGGL((commit_kernel<F, S>), grid, block, lds, stream, S0, U, k, alpha, path, path_len, L_max, \
                        parent, N, H, S_new, err)

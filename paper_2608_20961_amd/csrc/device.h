@@ -10,6 +10,8 @@ namespace treewy {
 
 constexpr int D = 128;          // d_k == d_v
 constexpr int THREADS = 256;    // four wave64s per workgroup
+constexpr int MAX_TREE = 256;   // most nodes per draft tree (one 64-bit ancestor word per 64 nodes)
+constexpr int MASK_WORDS = MAX_TREE / 64;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));

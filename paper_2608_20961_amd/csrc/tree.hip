@@ -53,33 +53,55 @@ __global__ __launch_bounds__(THREADS) void accept_greedy_kernel(
     const int32_t *__restrict__ target, const int32_t *__restrict__ root, int N, int B, int L_max,
     int32_t *__restrict__ path, int32_t *__restrict__ path_len, int32_t *__restrict__ bonus,
     int32_t *__restrict__ err) {
+    constexpr int W = MAX_TREE / 64;                     // nodes per lane: lane + 64 w
     const int lane = threadIdx.x & 63;
     const int b = blockIdx.x * (THREADS / 64) + (threadIdx.x >> 6);
     if (b >= B) return;                                  // whole waves leave together
     const size_t row = (size_t)b * N;
-    int par = -1, tok = 0, pred = 0;
-    if (lane < N) {
-        par = parent[row + lane];
-        tok = draft[row + lane];
-        pred = target[row + lane];
-        if (par < -1 || par >= lane) {
-            flag_error(err, b, TREEWY_FLAG_BAD_PARENT);
-            par = -1;
+    int par[W], tok[W], pred[W];
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+        const int t = lane + 64 * w;
+        par[w] = -1;
+        tok[w] = pred[w] = 0;
+        if (t < N) {
+            par[w] = parent[row + t];
+            tok[w] = draft[row + t];
+            pred[w] = target[row + t];
+            if (par[w] < -1 || par[w] >= t) {
+                flag_error(err, b, TREEWY_FLAG_BAD_PARENT);
+                par[w] = -1;
+            }
         }
     }
-    int pos = -1, want = root[b], len = 0, mine = -1;    // lane l keeps the l-th accepted node
+    int pos = -1, want = root[b], len = 0;
+    int mine[W];                                         // entry lane + 64 w of the accepted path
+#pragma unroll
+    for (int w = 0; w < W; ++w) mine[w] = -1;
     while (true) {
-        const uint64_t m = __ballot(lane < N && par == pos && tok == want);
-        if (m == 0) break;
-        const int c = __builtin_ctzll(m);
-        if (lane == len) mine = c;
+        int c = -1;                                      // lowest-index matching child of pos
+#pragma unroll
+        for (int w = 0; w < W; ++w) {
+            const uint64_t m = __ballot(lane + 64 * w < N && par[w] == pos && tok[w] == want);
+            if (c < 0 && m != 0) c = 64 * w + __builtin_ctzll(m);
+        }
+        if (c < 0) break;
+#pragma unroll
+        for (int w = 0; w < W; ++w) {
+            if (lane + 64 * w == len) mine[w] = c;
+            const int p = __shfl(pred[w], c & 63);
+            if (w == (c >> 6)) want = p;
+        }
         ++len;
-        want = __shfl(pred, c);
         pos = c;
     }
     const bool fits = len <= L_max;
     if (!fits && lane == 0) flag_error(err, b, TREEWY_FLAG_BAD_PATH);
-    if (lane < L_max) path[(size_t)b * L_max + lane] = fits && lane < len ? mine : -1;
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+        const int l = lane + 64 * w;
+        if (l < L_max) path[(size_t)b * L_max + l] = fits && l < len ? mine[w] : -1;
+    }
     if (lane == 0) {
         path_len[b] = fits ? len : 0;
         if (bonus) bonus[b] = want;

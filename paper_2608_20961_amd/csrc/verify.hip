@@ -89,10 +89,19 @@ struct VerifyLds {
     static constexpr int KPT_OFF = META_OFF + 2 * META_BYTES;
     static constexpr int UWT_OFF = KPT_OFF + D * CL * (F32IN ? 4 : 2);
     static constexpr int BYTES = FUSE ? UWT_OFF + D * CL * 4 : BASE_BYTES;
+    // Trees of more than 64 nodes, walked in chunks of 64: every node's
+    // cumulative decay and ancestor mask (one word per chunk), and one
+    // earlier chunk's keys staged like K.
+    static constexpr int GALL_OFF = BASE_BYTES;
+    static constexpr int ANCALL_OFF = GALL_OFF + MAX_TREE * 4;
+    static constexpr int KJ_OFF = ANCALL_OFF + MAX_TREE * MASK_WORDS * 8;
+    static constexpr int KJLO_OFF = KJ_OFF + NP * XS * 2;
+    static constexpr int TREE_BYTES = KJLO_OFF + (F32IN ? NP * XS * 2 : 0);
     static_assert(NP * US * 4 <= B_OFF, "U staging must fit where K/Q were staged");
     static_assert(B_OFF % 16 == 0 && A_OFF % 16 == 0 && BETA_OFF % 16 == 0 && G_OFF % 16 == 0 &&
                   ANC_OFF % 32 == 0 && O_OFF % 16 == 0 && V_OFF % 16 == 0 &&
-                  KPT_OFF % 16 == 0 && UWT_OFF % 16 == 0, "alignment");
+                  KPT_OFF % 16 == 0 && UWT_OFF % 16 == 0 && ANCALL_OFF % 16 == 0 && KJ_OFF % 16 == 0 &&
+                  KJLO_OFF % 16 == 0, "alignment");
 };
 
 // One unit's HBM reads, held in registers from issue to use.  Every read goes
@@ -155,11 +164,11 @@ struct UnitReads {
     }
 
     __device__ __forceinline__ void issue(const void *S0, const In *q, const In *k, const In *vv,
-                                          const float *alpha, const float *beta, const int32_t *parent,
-                                          int u, int b, int N, size_t node0, bool load_state, int tid,
+                                          const float *alpha, const float *beta, const int32_t *prow,
+                                          int u, int N, size_t node0, bool load_state, int tid,
                                           int lane, int wave, int hg, int col) {
-        if (wave == 0) {
-            par = parent ? ld_i32(make_rsrc(parent + (size_t)b * N, N * 4), lane * 4) : lane - 1;
+        if (wave == 0) {                                // prow: this unit's parents of the N nodes (null: a chain)
+            par = prow ? ld_i32(make_rsrc(prow, N * 4), lane * 4) : lane - 1;
             al = ld_f32(make_rsrc(alpha + node0, N * 4), lane * 4);
             be = ld_f32(make_rsrc(beta + node0, N * 4), lane * 4);
         }
@@ -228,18 +237,25 @@ __device__ __forceinline__ void sweep_column(float (&r)[NP], const float *Bm, in
     }
 }
 
-// Two workgroups per CU where 256 registers per lane suffice.  The chain
-// prefill keeps the state in registers through the whole chunk, which needs
-// the full register file (one workgroup per CU); so do fp32 inputs at 64 nodes.
-template <int NP, bool F32IN, bool FUSE, bool SBF, bool PRE>
-__global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || PRE) ? 1 : 2) void verify_kernel(
+// How a unit's nodes are walked: in one pass (at most 64 nodes), as a chain
+// in chunks of 64 tokens with the state carried between chunks (chain
+// prefill), or as a tree of more than 64 nodes in chunks of 64, S0 held
+// throughout and each chunk coupled to the earlier ones.
+constexpr int ONE_PASS = 0, CHAIN_PREFILL = 1, TREE_CHUNKS = 2;
+
+// Two workgroups per CU where 256 registers per lane suffice.  The chunked
+// modes keep the state in registers from chunk to chunk, which needs the
+// full register file (one workgroup per CU); so do fp32 inputs at 64 nodes.
+template <int NP, bool F32IN, bool FUSE, bool SBF, int MODE>
+__global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || MODE != ONE_PASS) ? 1 : 2) void verify_kernel(
     const void *S0, const void *__restrict__ q_, const void *__restrict__ k_,
     const void *__restrict__ v_, const float *__restrict__ alpha, const float *__restrict__ beta,
     const int32_t *__restrict__ parent, int N_all, int in_stride, int u_stride, int H, int units,
     void *__restrict__ o_, float *U, int32_t *__restrict__ err, CommitArgs cm) {
     using In = typename std::conditional<F32IN, float, __bf16>::type;
     static_assert(!(SBF && F32IN), "a bf16 state is paired with bf16 inputs");
-    static_assert(!(PRE && (FUSE || NP != 64)), "the chain prefill runs 64-token chunks, unfused");
+    constexpr bool PRE = MODE == CHAIN_PREFILL, XT = MODE == TREE_CHUNKS;
+    static_assert(!(MODE != ONE_PASS && (FUSE || NP != 64)), "chunked modes run 64-node chunks, unfused");
     using L = VerifyLds<NP, F32IN, FUSE>;
     using Reads = UnitReads<NP, F32IN, FUSE, SBF>;
     constexpr int SB = Reads::SB;
@@ -247,7 +263,7 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || PRE) ? 1 : 2) void
     constexpr int XS = L::XS, MS = L::MS, US = L::US, OS = L::OS;
     constexpr int CHUNK = Reads::CHUNK, CPR = Reads::CPR, KQN = Reads::KQN;
 
-    __shared__ __attribute__((aligned(16))) unsigned char lds[L::BYTES];
+    __shared__ __attribute__((aligned(16))) unsigned char lds[XT ? L::TREE_BYTES : L::BYTES];
     __bf16 *Xh = reinterpret_cast<__bf16 *>(lds);
     __bf16 *Xl = reinterpret_cast<__bf16 *>(lds + L::XLO_OFF);
     float *Bm = reinterpret_cast<float *>(lds + L::B_OFF);
@@ -258,6 +274,10 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || PRE) ? 1 : 2) void
     float *g_s = reinterpret_cast<float *>(lds + L::G_OFF);
     uint64_t *anc_s = reinterpret_cast<uint64_t *>(lds + L::ANC_OFF);
     int *shallow_s = reinterpret_cast<int *>(lds + L::FLAG_OFF);
+    float *g_all = reinterpret_cast<float *>(lds + L::GALL_OFF);            // (tree chunks)
+    uint64_t *anc_all = reinterpret_cast<uint64_t *>(lds + L::ANCALL_OFF);
+    __bf16 *Kj = reinterpret_cast<__bf16 *>(lds + L::KJ_OFF);
+    __bf16 *Kjl = reinterpret_cast<__bf16 *>(lds + L::KJLO_OFF);
     constexpr int FAST = 8;                              // ancestors a lane holds in registers
     // fused commit staging (unused otherwise)
     constexpr int CL = L::CL;
@@ -329,11 +349,13 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || PRE) ? 1 : 2) void
         const int l32 = lane & 31, hg = lane >> 5;
         const int col = wave * 32 + l32;                 // this lane's d_v column (= row of S0)
         const int b = u / H;
-        // Chain prefill: the unit's tokens in chunks of 64, the state kept in
+        // Chunked modes: the unit's nodes in chunks of 64, the state kept in
         // registers from one chunk to the next.  Otherwise one pass.
-        const int chunks = PRE ? (N_all + 63) / 64 : 1;
+        const int chunks = MODE != ONE_PASS ? (N_all + 63) / 64 : 1;
         for (int chunk = 0; chunk < chunks; ++chunk) {
-        const int N = PRE ? (N_all - 64 * chunk < 64 ? N_all - 64 * chunk : 64) : N_all;
+        const int N = MODE != ONE_PASS ? (N_all - 64 * chunk < 64 ? N_all - 64 * chunk : 64) : N_all;
+        const int base = XT ? 64 * chunk : 0;            // tree index of this chunk's node 0
+        const int32_t *prow = parent ? parent + (size_t)b * N_all + base : nullptr;
         const size_t node0 = (size_t)u * in_stride + 64 * chunk;   // row of node 0 in q/k/v/alpha/beta/o
         const size_t unode0 = (size_t)u * u_stride;      // ... and in U
 
@@ -385,7 +407,7 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || PRE) ? 1 : 2) void
         }
         constexpr bool AHEAD = PRE && !F32IN;            // prefill fetches the next chunk early (bf16 inputs)
         if (!AHEAD || chunk == 0)                        // (then later chunks were fetched one chunk ahead)
-            rd.issue(S0, q, k, v, alpha, beta, parent, u, b, N, node0, chunk == 0, tid, lane, wave, hg, col);
+            rd.issue(S0, q, k, v, alpha, beta, prow, u, N, node0, chunk == 0, tid, lane, wave, hg, col);
 
         // ---- phase 1: ancestors and cumulative decay by pointer jumping ----
         // Lane t of wave 0 keeps (ptr, prod, mask): ptr an ancestor of t (or
@@ -393,29 +415,56 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || PRE) ? 1 : 2) void
         // ancestors of t strictly below t down to and including ptr.  Each
         // round doubles the covered path by reading the state of lane ptr, so
         // depth d needs ceil(log2 d) rounds; then prod = g_t, mask = ancestors.
+        // Tree chunks: a parent in an earlier chunk already has its final
+        // decay and ancestors (g_all, anc_all), so the lane takes them over
+        // at once; ext holds the ancestor words of the earlier chunks.
         if (wave == 0) {
             int ptr = lane < N ? rd.par : -1;
-            if (lane < N && (ptr < -1 || ptr >= lane)) {
+            if (lane < N && (ptr < -1 || ptr >= base + lane)) {
                 flag_error(err, b, TREEWY_FLAG_BAD_PARENT);
                 ptr = -1;
             }
             float prod = lane < N ? rd.al : 0.f;
+            uint64_t ext[XT ? MASK_WORDS : 1] = {};
+            if constexpr (XT) {
+                if (ptr >= 0 && ptr < base) {
+                    prod *= g_all[ptr];
+#pragma unroll
+                    for (int j = 0; j < MASK_WORDS; ++j)
+                        ext[j] = anc_all[ptr * MASK_WORDS + j] | (j == (ptr >> 6) ? 1ull << (ptr & 63) : 0ull);
+                    ptr = -1;
+                } else if (ptr >= 0) {
+                    ptr -= base;
+                }
+            }
             uint64_t mask = ptr >= 0 ? (1ull << ptr) : 0ull;
             while (__any(ptr >= 0)) {
                 const int src = ptr >= 0 ? ptr : lane;
                 const float prod_s = __shfl(prod, src);
                 const int ptr_s = __shfl(ptr, src);
                 const uint64_t mask_s = __shfl(mask, src);
+                uint64_t ext_s[XT ? MASK_WORDS : 1] = {};
+                if constexpr (XT)
+#pragma unroll
+                    for (int j = 0; j < MASK_WORDS; ++j) ext_s[j] = __shfl(ext[j], src);
                 if (ptr >= 0) {
                     prod *= prod_s;
                     mask |= mask_s;
                     ptr = ptr_s;
+                    if constexpr (XT)
+#pragma unroll
+                        for (int j = 0; j < MASK_WORDS; ++j) ext[j] |= ext_s[j];
                 }
             }
             if (lane < NP) {
                 g_s[lane] = prod;
                 be_s[lane] = lane < N ? rd.be : 0.f;
                 anc_s[lane] = mask;
+            }
+            if constexpr (XT) {                          // base + lane < MAX_TREE: at most 4 chunks
+                g_all[base + lane] = prod;
+#pragma unroll
+                for (int j = 0; j < MASK_WORDS; ++j) anc_all[(base + lane) * MASK_WORDS + j] = j == chunk ? mask : ext[j];
             }
             const bool shallow = !__any(__popcll(mask) > FAST);
             if (lane == 0) *shallow_s = shallow ? 1 : 0;
@@ -428,13 +477,10 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || PRE) ? 1 : 2) void
         }
         // K and Q into LDS as bf16 (hi/lo for fp32 input), padding rows zero,
         // with the d_k order permuted by kperm (see UnitReads::kperm).
-#pragma unroll
-        for (int i = 0; i < KQN; ++i) {
-            const int idx = tid + THREADS * i, r = idx / CPR, c = (idx % CPR) * CHUNK;
-            const uint4 val = rd.kq[i];
+        auto stage_x = [&](__bf16 *xh, __bf16 *xl, int r, int c, const uint4 &val) {
             if constexpr (!F32IN) {
-                *reinterpret_cast<uint2 *>(Xh + r * XS + Reads::kperm(c)) = make_uint2(val.x, val.y);
-                *reinterpret_cast<uint2 *>(Xh + r * XS + Reads::kperm(c + 4)) = make_uint2(val.z, val.w);
+                *reinterpret_cast<uint2 *>(xh + r * XS + Reads::kperm(c)) = make_uint2(val.x, val.y);
+                *reinterpret_cast<uint2 *>(xh + r * XS + Reads::kperm(c + 4)) = make_uint2(val.z, val.w);
             } else {
                 const f32x4 f = *reinterpret_cast<const f32x4 *>(&val);
                 bf16x4 hi, lo;
@@ -443,9 +489,14 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || PRE) ? 1 : 2) void
                     hi[e] = (__bf16)f[e];
                     lo[e] = (__bf16)(f[e] - (float)hi[e]);
                 }
-                *reinterpret_cast<bf16x4 *>(Xh + r * XS + Reads::kperm(c)) = hi;
-                *reinterpret_cast<bf16x4 *>(Xl + r * XS + Reads::kperm(c)) = lo;
+                *reinterpret_cast<bf16x4 *>(xh + r * XS + Reads::kperm(c)) = hi;
+                *reinterpret_cast<bf16x4 *>(xl + r * XS + Reads::kperm(c)) = lo;
             }
+        };
+#pragma unroll
+        for (int i = 0; i < KQN; ++i) {
+            const int idx = tid + THREADS * i, r = idx / CPR, c = (idx % CPR) * CHUNK;
+            stage_x(Xh, Xl, r, c, rd.kq[i]);
         }
         // V rows into LDS as loaded (rows of padding nodes are zero).
         {
@@ -479,7 +530,88 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || PRE) ? 1 : 2) void
         if constexpr (AHEAD) {
             if (chunk + 1 < chunks) {
                 const int N1 = N_all - 64 * (chunk + 1) < 64 ? N_all - 64 * (chunk + 1) : 64;
-                rd.issue(S0, q, k, v, alpha, beta, parent, u, b, N1, node0 + 64, false, tid, lane, wave, hg, col);
+                rd.issue(S0, q, k, v, alpha, beta, nullptr, u, N1, node0 + 64, false, tid, lane, wave, hg, col);
+            }
+        }
+
+        // ---- tree chunks: coupling to the earlier chunks ------------------
+        // For t in this chunk and i in an earlier chunk j, B[t, i] U_i and
+        // A[t, i] U_i enter eq. 2 through R and O; with B[t, i] =
+        // beta_t (g_t / g_i) k_t . k_i and A[t, i] = (g_t / g_i) q_t . k_i
+        // (i an ancestor of t), both are g_t times
+        //   sum over ancestors i in chunk j of ((x_t . k_i) / g_i) U_i,  x = k or q,
+        // which is added to [K; Q] S0^T before phase 4 scales by g_t (and
+        // beta_t for R).  Per chunk j: K_j is staged in LDS, the cross gram
+        // [K; Q] K_j^T is masked and scaled into the B and A areas (free until
+        // phase 2), and the product with U_j (written by this workgroup one
+        // or more chunks ago) is accumulated on the matrix cores.
+        f32x16 accp[2 * MT];
+        if constexpr (XT) {
+#pragma unroll
+            for (int m = 0; m < 2 * MT; ++m) accp[m] = f32x16{};
+            for (int j = 0; j < chunk; ++j) {            // uniform loop
+                const rsrc_t rkj = make_rsrc(k + ((size_t)u * in_stride + 64 * j) * D, 64 * Reads::ROW);
+#pragma unroll
+                for (int i = 0; i < Reads::KN; ++i) {
+                    const int idx = tid + THREADS * i, r = idx / CPR, c = (idx % CPR) * CHUNK;
+                    stage_x(Kj, Kjl, r, c, ld_u32x4<CACHED>(rkj, r * Reads::ROW + c * (int)sizeof(In)));
+                }
+                __syncthreads();
+                {
+                    const int mt = wave >> 1, nt = wave & 1;     // one 32 x 32 tile per wave
+                    f32x16 gkk = {}, gqk = {};
+                    const int ak = (32 * mt + l32) * XS + 8 * hg, aq = (NP + 32 * mt + l32) * XS + 8 * hg;
+                    const int bk = (32 * nt + l32) * XS + 8 * hg;
+#pragma unroll 2
+                    for (int s = 0; s < 8; ++s) {
+                        const bf16x8 a_k = *reinterpret_cast<const bf16x8 *>(Xh + ak + 16 * s);
+                        const bf16x8 a_q = *reinterpret_cast<const bf16x8 *>(Xh + aq + 16 * s);
+                        const bf16x8 b_k = *reinterpret_cast<const bf16x8 *>(Kj + bk + 16 * s);
+                        gkk = mma(a_k, b_k, gkk);
+                        gqk = mma(a_q, b_k, gqk);
+                        if constexpr (F32IN) {
+                            const bf16x8 a_kl = *reinterpret_cast<const bf16x8 *>(Xl + ak + 16 * s);
+                            const bf16x8 a_ql = *reinterpret_cast<const bf16x8 *>(Xl + aq + 16 * s);
+                            const bf16x8 b_kl = *reinterpret_cast<const bf16x8 *>(Kjl + bk + 16 * s);
+                            gkk = mma(a_k, b_kl, gkk);
+                            gkk = mma(a_kl, b_k, gkk);
+                            gqk = mma(a_q, b_kl, gqk);
+                            gqk = mma(a_ql, b_k, gqk);
+                        }
+                    }
+                    const int i = 32 * nt + l32;
+                    const float inv_gi = 1.f / g_all[64 * j + i];   // every node of an earlier chunk is real
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int t = 32 * mt + acc_row(r, hg);
+                        const bool a = (anc_all[(base + t) * MASK_WORDS + j] >> i) & 1ull;
+                        Bm[t * MS + i] = a ? gkk[r] * inv_gi : 0.f;
+                        Am[t * MS + i] = a ? gqk[r] * inv_gi : 0.f;
+                    }
+                }
+                __syncthreads();
+                const rsrc_t ruj = make_rsrc(U + ((size_t)u * u_stride + 64 * j) * D, 64 * D * 4);
+#pragma unroll
+                for (int s = 0; s < 4; ++s) {
+                    float ub[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) ub[e] = ld_f32(ruj, ((16 * s + 8 * hg + e) * D + col) * 4);
+                    bf16x8 bh, bl;
+                    split8(ub, bh, bl);
+#pragma unroll
+                    for (int m = 0; m < 2 * MT; ++m) {
+                        const float *crow = (m < MT ? Bm : Am) + (32 * (m % MT) + l32) * MS + 16 * s + 8 * hg;
+                        float c8[8];
+                        *reinterpret_cast<f32x4 *>(c8) = *reinterpret_cast<const f32x4 *>(crow);
+                        *reinterpret_cast<f32x4 *>(c8 + 4) = *reinterpret_cast<const f32x4 *>(crow + 4);
+                        bf16x8 ah, alo;
+                        split8(c8, ah, alo);
+                        accp[m] = mma(ah, bh, accp[m]);
+                        accp[m] = mma(ah, bl, accp[m]);
+                        accp[m] = mma(alo, bh, accp[m]);
+                    }
+                }
+                __syncthreads();                         // the B and A areas and K_j are rewritten next
             }
         }
 
@@ -717,9 +849,9 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || PRE) ? 1 : 2) void
         // The A operands (rows of [K; Q] in LDS) are double-buffered one
         // K-step ahead; the scheduling barriers keep the compiler from
         // hoisting every step's operands at once.
-        f32x16 accp[2 * MT];
+        if constexpr (!XT)
 #pragma unroll
-        for (int m = 0; m < 2 * MT; ++m) accp[m] = f32x16{};
+            for (int m = 0; m < 2 * MT; ++m) accp[m] = f32x16{};
         {
             // (one buffer in the fused variant, whose update block needs the registers)
             constexpr int NBUF = FUSE ? 1 : 2;
@@ -826,7 +958,7 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || PRE) ? 1 : 2) void
             __builtin_amdgcn_sched_barrier(0);
         }
         __syncthreads();                                 // every wave is done reading T
-        const rsrc_t ru = make_rsrc(PRE ? nullptr : U + unode0 * D, PRE ? 0 : N * D * 4);
+        const rsrc_t ru = make_rsrc(PRE ? nullptr : U + (unode0 + base) * D, PRE ? 0 : N * D * 4);
         const rsrc_t ro = make_rsrc(o + node0 * D, N * D * (int)sizeof(In));
         if constexpr (!PRE) {                            // (the chain prefill keeps U in registers and K in LDS)
 #pragma unroll
@@ -928,6 +1060,9 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || PRE) ? 1 : 2) void
                 }
             }
         }
+        // (Tree chunks read this chunk's U rows back in later chunks: the
+        // barrier makes a workgroup's global stores visible to its own later
+        // loads, with no cache maintenance at workgroup scope.)
         __syncthreads();                                 // LDS is rewritten by the next unit / chunk
         }                                                // chunk
         if constexpr (PRE) {                             // the state after the unit's last token
@@ -948,7 +1083,7 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || PRE) ? 1 : 2) void
 
 namespace {
 
-template <int NP, bool F32IN, bool FUSE, bool SBF, bool PRE = false>
+template <int NP, bool F32IN, bool FUSE, bool SBF, int MODE = ONE_PASS>
 int resident_grid(int units) {
     static int per_device[64] = {0};
     int dev = 0;
@@ -957,7 +1092,7 @@ int resident_grid(int units) {
         int cus = 0, blocks = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
             cus = 256;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, verify_kernel<NP, F32IN, FUSE, SBF, PRE>, THREADS,
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, verify_kernel<NP, F32IN, FUSE, SBF, MODE>, THREADS,
                                                          0) != hipSuccess ||
             blocks <= 0)
             blocks = 1;
@@ -966,13 +1101,13 @@ int resident_grid(int units) {
     return units < per_device[dev] ? units : per_device[dev];
 }
 
-template <int NP, bool F32IN, bool FUSE, bool SBF, bool PRE = false>
+template <int NP, bool F32IN, bool FUSE, bool SBF, int MODE = ONE_PASS>
 hipError_t launch(const void *S0, const void *q, const void *k, const void *v, const float *alpha,
                   const float *beta, const int32_t *parent, int N, int in_stride, int u_stride, int B, int H,
                   void *o, float *U, int32_t *err, const CommitArgs &cm, hipStream_t stream) {
     const int units = B * H;
-    hipLaunchKernelGGL((verify_kernel<NP, F32IN, FUSE, SBF, PRE>),
-                       dim3((unsigned)resident_grid<NP, F32IN, FUSE, SBF, PRE>(units)), dim3(THREADS), 0, stream,
+    hipLaunchKernelGGL((verify_kernel<NP, F32IN, FUSE, SBF, MODE>),
+                       dim3((unsigned)resident_grid<NP, F32IN, FUSE, SBF, MODE>(units)), dim3(THREADS), 0, stream,
                        S0, q, k, v, alpha, beta, parent, N, in_stride, u_stride, H, units, o, U, err, cm);
     return hipGetLastError();
 }
@@ -998,6 +1133,16 @@ hipError_t launch_verify(const void *S0, const void *q, const void *k, const voi
                          int B, int H, bool f32_in, bool bf16_state, void *o, float *U, int32_t *err,
                          hipStream_t stream) {
     const CommitArgs none = {};
+    if (N > 64) {                                        // trees of more than 64 nodes: chunks of 64
+        if (bf16_state)
+            return launch<64, false, false, true, TREE_CHUNKS>(S0, q, k, v, alpha, beta, parent, N, N, N, B, H, o, U,
+                                                                err, none, stream);
+        if (f32_in)
+            return launch<64, true, false, false, TREE_CHUNKS>(S0, q, k, v, alpha, beta, parent, N, N, N, B, H, o, U,
+                                                                err, none, stream);
+        return launch<64, false, false, false, TREE_CHUNKS>(S0, q, k, v, alpha, beta, parent, N, N, N, B, H, o, U,
+                                                             err, none, stream);
+    }
     return dispatch<false>(S0, q, k, v, alpha, beta, parent, N, N, N, B, H, f32_in, bf16_state, o, U, err, none,
                            stream);
 }
@@ -1022,12 +1167,12 @@ hipError_t launch_prefill(const void *S0, const void *q, const void *k, const vo
     CommitArgs cm = {};
     cm.S_new = S_T;
     if (bf16_state)
-        return launch<64, false, false, true, true>(S0, q, k, v, alpha, beta, nullptr, T, T, 0, B, H, o, nullptr,
+        return launch<64, false, false, true, CHAIN_PREFILL>(S0, q, k, v, alpha, beta, nullptr, T, T, 0, B, H, o, nullptr,
                                                    err, cm, stream);
     if (f32_in)
-        return launch<64, true, false, false, true>(S0, q, k, v, alpha, beta, nullptr, T, T, 0, B, H, o, nullptr,
+        return launch<64, true, false, false, CHAIN_PREFILL>(S0, q, k, v, alpha, beta, nullptr, T, T, 0, B, H, o, nullptr,
                                                    err, cm, stream);
-    return launch<64, false, false, false, true>(S0, q, k, v, alpha, beta, nullptr, T, T, 0, B, H, o, nullptr, err,
+    return launch<64, false, false, false, CHAIN_PREFILL>(S0, q, k, v, alpha, beta, nullptr, T, T, 0, B, H, o, nullptr, err,
                                                 cm, stream);
 }
 

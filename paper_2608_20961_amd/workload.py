@@ -77,6 +77,11 @@ WORKLOADS: Dict[int, Workload] = {
                 (0.85, 0.999), (0.05, 0.95), 256, "uniform_node"),
 }
 
+# Trees past one 64-node chunk, at the 397B layer shape: the distributions of
+# the 64-node tree, twice the nodes and twice the depth.
+BIG_TREE = Workload("397B-tree128", 128, 64, 128, 128, 128, "bf16", "tree", 16, (4, 4, 2),
+                    (0.9, 0.999), (0.05, 0.95), 256, "uniform_node")
+
 
 def scaled(w: Workload, B: Optional[int] = None, H: Optional[int] = None,
            N: Optional[int] = None) -> Workload:

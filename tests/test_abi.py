@@ -55,7 +55,8 @@ def _verify(tw, fn="treewy_verify", S0=A, q=A, N=8, B=2, H=2, dk=128, dv=128, dt
 def test_verify_host_checks(tw, fn):
     assert _verify(tw, fn, dk=64) == tw.TREEWY_ERR_UNSUPPORTED
     assert _verify(tw, fn, dv=96) == tw.TREEWY_ERR_UNSUPPORTED
-    assert _verify(tw, fn, N=65) == tw.TREEWY_ERR_UNSUPPORTED
+    # verify walks trees of up to 256 nodes in chunks; the snapshot baseline stops at 64
+    assert _verify(tw, fn, N=257 if fn == "treewy_verify" else 65) == tw.TREEWY_ERR_UNSUPPORTED
     assert _verify(tw, fn, N=-1) == tw.TREEWY_ERR_INVALID_ARG
     assert _verify(tw, fn, B=-3) == tw.TREEWY_ERR_INVALID_ARG
     assert _verify(tw, fn, dt=7) == tw.TREEWY_ERR_INVALID_ARG
@@ -78,7 +79,8 @@ def test_commit_host_checks(tw):
         return f(S0, A, A, A, path, plen, L_max, None, N, B, H, dk, 128, dt, st, S_new, None, None)
 
     assert call(dk=64) == tw.TREEWY_ERR_UNSUPPORTED
-    assert call(L_max=65) == tw.TREEWY_ERR_UNSUPPORTED
+    assert call(L_max=257) == tw.TREEWY_ERR_UNSUPPORTED
+    assert call(N=257) == tw.TREEWY_ERR_UNSUPPORTED
     assert call(L_max=-1) == tw.TREEWY_ERR_INVALID_ARG
     assert call(plen=None) == tw.TREEWY_ERR_INVALID_ARG
     assert call(path=None) == tw.TREEWY_ERR_INVALID_ARG
@@ -122,7 +124,8 @@ def test_commit_verify_host_checks(tw):
 def test_snapshot_commit_and_path_host_checks(tw):
     assert tw.lib.treewy_snapshot_commit(A, A, None, 8, 2, 2, 128, 128, A, None, None) == tw.TREEWY_ERR_INVALID_ARG
     assert tw.lib.treewy_snapshot_commit(A, A, A, 8, 2, 2, 128, 64, A, None, None) == tw.TREEWY_ERR_UNSUPPORTED
-    assert tw.lib.treewy_path_from_node(A, A, 65, 2, 8, A, A, None, None) == tw.TREEWY_ERR_UNSUPPORTED
+    assert tw.lib.treewy_path_from_node(A, A, 257, 2, 8, A, A, None, None) == tw.TREEWY_ERR_UNSUPPORTED
+    assert tw.lib.treewy_path_from_node(A, A, 8, 2, 257, A, A, None, None) == tw.TREEWY_ERR_UNSUPPORTED
     assert tw.lib.treewy_path_from_node(A, None, 8, 2, 8, A, A, None, None) == tw.TREEWY_ERR_INVALID_ARG
     assert tw.lib.treewy_path_from_node(None, None, 8, 0, 8, None, None, None, None) == tw.TREEWY_OK
 
@@ -133,8 +136,8 @@ def test_accept_greedy_host_checks(tw):
     def call(parent=A, draft=A, target=A, root=A, N=8, B=2, L_max=8, path=A, plen=A):
         return f(parent, draft, target, root, N, B, L_max, path, plen, None, None, None)
 
-    assert call(N=65) == tw.TREEWY_ERR_UNSUPPORTED
-    assert call(L_max=65) == tw.TREEWY_ERR_UNSUPPORTED
+    assert call(N=257) == tw.TREEWY_ERR_UNSUPPORTED
+    assert call(L_max=257) == tw.TREEWY_ERR_UNSUPPORTED
     assert call(N=-1) == tw.TREEWY_ERR_INVALID_ARG
     assert call(B=-1) == tw.TREEWY_ERR_INVALID_ARG
     assert call(root=None) == tw.TREEWY_ERR_INVALID_ARG
