@@ -90,18 +90,15 @@ struct VerifyLds {
     static constexpr int UWT_OFF = KPT_OFF + D * CL * (F32IN ? 4 : 2);
     static constexpr int BYTES = FUSE ? UWT_OFF + D * CL * 4 : BASE_BYTES;
     // Trees of more than 64 nodes, walked in chunks of 64: every node's
-    // cumulative decay and ancestor mask (one word per chunk), and one
-    // earlier chunk's keys staged like K.
+    // cumulative decay and ancestor mask (one word per chunk).  With bf16
+    // inputs this still fits two workgroups per CU.
     static constexpr int GALL_OFF = BASE_BYTES;
     static constexpr int ANCALL_OFF = GALL_OFF + MAX_TREE * 4;
-    static constexpr int KJ_OFF = ANCALL_OFF + MAX_TREE * MASK_WORDS * 8;
-    static constexpr int KJLO_OFF = KJ_OFF + NP * XS * 2;
-    static constexpr int TREE_BYTES = KJLO_OFF + (F32IN ? NP * XS * 2 : 0);
+    static constexpr int TREE_BYTES = ANCALL_OFF + MAX_TREE * MASK_WORDS * 8;
     static_assert(NP * US * 4 <= B_OFF, "U staging must fit where K/Q were staged");
     static_assert(B_OFF % 16 == 0 && A_OFF % 16 == 0 && BETA_OFF % 16 == 0 && G_OFF % 16 == 0 &&
                   ANC_OFF % 32 == 0 && O_OFF % 16 == 0 && V_OFF % 16 == 0 &&
-                  KPT_OFF % 16 == 0 && UWT_OFF % 16 == 0 && ANCALL_OFF % 16 == 0 && KJ_OFF % 16 == 0 &&
-                  KJLO_OFF % 16 == 0, "alignment");
+                  KPT_OFF % 16 == 0 && UWT_OFF % 16 == 0 && ANCALL_OFF % 16 == 0, "alignment");
 };
 
 // One unit's HBM reads, held in registers from issue to use.  Every read goes
@@ -163,6 +160,8 @@ struct UnitReads {
         else s0[s][h] = x;
     }
 
+    // KQP: cache policy of the K/Q rows (tree chunks read them again).
+    template <int KQP = STREAM>
     __device__ __forceinline__ void issue(const void *S0, const In *q, const In *k, const In *vv,
                                           const float *alpha, const float *beta, const int32_t *prow,
                                           int u, int N, size_t node0, bool load_state, int tid,
@@ -178,12 +177,15 @@ struct UnitReads {
         for (int i = 0; i < KQN; ++i) {
             const int idx = tid + THREADS * i, r = idx / CPR, c = (idx % CPR) * CHUNK;
             const int t = i < KN ? r : r - NP;
-            kq[i] = ld_u32x4<STREAM>(i < KN ? rk : rq, t * ROW + c * (int)sizeof(In));
+            kq[i] = ld_u32x4<KQP>(i < KN ? rk : rq, t * ROW + c * (int)sizeof(In));
         }
         const rsrc_t rv = make_rsrc(vv + node0 * D, N * ROW);
 #pragma unroll
         for (int i = 0; i < VQN; ++i) vq[i] = ld_u32x4<STREAM>(rv, (tid + THREADS * i) * 16);
-        if (!load_state) return;                        // (chain prefill: the state is already in registers)
+        if (load_state) issue_state(S0, u, hg, col);    // (chain prefill: the state is already in registers)
+    }
+
+    __device__ __forceinline__ void issue_state(const void *S0, int u, int hg, int col) {
         const rsrc_t rs = make_rsrc(static_cast<const char *>(S0) + (size_t)u * D * D * SB, D * D * SB);
         const int base = (col * D + 4 * hg) * SB;
 #pragma unroll
@@ -239,15 +241,15 @@ __device__ __forceinline__ void sweep_column(float (&r)[NP], const float *Bm, in
 
 // How a unit's nodes are walked: in one pass (at most 64 nodes), as a chain
 // in chunks of 64 tokens with the state carried between chunks (chain
-// prefill), or as a tree of more than 64 nodes in chunks of 64, S0 held
-// throughout and each chunk coupled to the earlier ones.
+// prefill), or as a tree of more than 64 nodes in chunks of 64, each chunk
+// reading S0 again and coupled to the earlier chunks.
 constexpr int ONE_PASS = 0, CHAIN_PREFILL = 1, TREE_CHUNKS = 2;
 
-// Two workgroups per CU where 256 registers per lane suffice.  The chunked
-// modes keep the state in registers from chunk to chunk, which needs the
+// Two workgroups per CU where 256 registers per lane suffice.  The chain
+// prefill keeps the state in registers from chunk to chunk, which needs the
 // full register file (one workgroup per CU); so do fp32 inputs at 64 nodes.
 template <int NP, bool F32IN, bool FUSE, bool SBF, int MODE>
-__global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || MODE != ONE_PASS) ? 1 : 2) void verify_kernel(
+__global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || MODE == CHAIN_PREFILL) ? 1 : 2) void verify_kernel(
     const void *S0, const void *__restrict__ q_, const void *__restrict__ k_,
     const void *__restrict__ v_, const float *__restrict__ alpha, const float *__restrict__ beta,
     const int32_t *__restrict__ parent, int N_all, int in_stride, int u_stride, int H, int units,
@@ -276,8 +278,6 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || MODE != ONE_PASS) 
     int *shallow_s = reinterpret_cast<int *>(lds + L::FLAG_OFF);
     float *g_all = reinterpret_cast<float *>(lds + L::GALL_OFF);            // (tree chunks)
     uint64_t *anc_all = reinterpret_cast<uint64_t *>(lds + L::ANCALL_OFF);
-    __bf16 *Kj = reinterpret_cast<__bf16 *>(lds + L::KJ_OFF);
-    __bf16 *Kjl = reinterpret_cast<__bf16 *>(lds + L::KJLO_OFF);
     constexpr int FAST = 8;                              // ancestors a lane holds in registers
     // fused commit staging (unused otherwise)
     constexpr int CL = L::CL;
@@ -342,17 +342,18 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || MODE != ONE_PASS) 
         __syncthreads();
     }
     for (int buf = 0; u < units; u += gridDim.x, buf ^= 1) {
-        // Lane indices are re-derived each iteration from an opaque copy so the
+        const int b = u / H;
+        // Chunked modes: the unit's nodes in chunks of 64 (the chain prefill
+        // keeps the state in registers from one chunk to the next).
+        // Otherwise one pass.
+        const int chunks = MODE != ONE_PASS ? (N_all + 63) / 64 : 1;
+        for (int chunk = 0; chunk < chunks; ++chunk) {
+        // Lane indices are re-derived each pass from an opaque copy so the
         // per-lane offsets below are recomputed here instead of being hoisted
-        // out of the loop and held in registers for its whole length.
+        // out of the loops and held in registers for their whole length.
         const int tid = opaque(threadIdx.x), lane = tid & 63;
         const int l32 = lane & 31, hg = lane >> 5;
         const int col = wave * 32 + l32;                 // this lane's d_v column (= row of S0)
-        const int b = u / H;
-        // Chunked modes: the unit's nodes in chunks of 64, the state kept in
-        // registers from one chunk to the next.  Otherwise one pass.
-        const int chunks = MODE != ONE_PASS ? (N_all + 63) / 64 : 1;
-        for (int chunk = 0; chunk < chunks; ++chunk) {
         const int N = MODE != ONE_PASS ? (N_all - 64 * chunk < 64 ? N_all - 64 * chunk : 64) : N_all;
         const int base = XT ? 64 * chunk : 0;            // tree index of this chunk's node 0
         const int32_t *prow = parent ? parent + (size_t)b * N_all + base : nullptr;
@@ -407,7 +408,8 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || MODE != ONE_PASS) 
         }
         constexpr bool AHEAD = PRE && !F32IN;            // prefill fetches the next chunk early (bf16 inputs)
         if (!AHEAD || chunk == 0)                        // (then later chunks were fetched one chunk ahead)
-            rd.issue(S0, q, k, v, alpha, beta, prow, u, N, node0, chunk == 0, tid, lane, wave, hg, col);
+            rd.template issue<XT ? CACHED : STREAM>(S0, q, k, v, alpha, beta, prow, u, N, node0, chunk == 0 || XT,
+                                                    tid, lane, wave, hg, col);
 
         // ---- phase 1: ancestors and cumulative decay by pointer jumping ----
         // Lane t of wave 0 keeps (ptr, prod, mask): ptr an ancestor of t (or
@@ -531,87 +533,6 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || MODE != ONE_PASS) 
             if (chunk + 1 < chunks) {
                 const int N1 = N_all - 64 * (chunk + 1) < 64 ? N_all - 64 * (chunk + 1) : 64;
                 rd.issue(S0, q, k, v, alpha, beta, nullptr, u, N1, node0 + 64, false, tid, lane, wave, hg, col);
-            }
-        }
-
-        // ---- tree chunks: coupling to the earlier chunks ------------------
-        // For t in this chunk and i in an earlier chunk j, B[t, i] U_i and
-        // A[t, i] U_i enter eq. 2 through R and O; with B[t, i] =
-        // beta_t (g_t / g_i) k_t . k_i and A[t, i] = (g_t / g_i) q_t . k_i
-        // (i an ancestor of t), both are g_t times
-        //   sum over ancestors i in chunk j of ((x_t . k_i) / g_i) U_i,  x = k or q,
-        // which is added to [K; Q] S0^T before phase 4 scales by g_t (and
-        // beta_t for R).  Per chunk j: K_j is staged in LDS, the cross gram
-        // [K; Q] K_j^T is masked and scaled into the B and A areas (free until
-        // phase 2), and the product with U_j (written by this workgroup one
-        // or more chunks ago) is accumulated on the matrix cores.
-        f32x16 accp[2 * MT];
-        if constexpr (XT) {
-#pragma unroll
-            for (int m = 0; m < 2 * MT; ++m) accp[m] = f32x16{};
-            for (int j = 0; j < chunk; ++j) {            // uniform loop
-                const rsrc_t rkj = make_rsrc(k + ((size_t)u * in_stride + 64 * j) * D, 64 * Reads::ROW);
-#pragma unroll
-                for (int i = 0; i < Reads::KN; ++i) {
-                    const int idx = tid + THREADS * i, r = idx / CPR, c = (idx % CPR) * CHUNK;
-                    stage_x(Kj, Kjl, r, c, ld_u32x4<CACHED>(rkj, r * Reads::ROW + c * (int)sizeof(In)));
-                }
-                __syncthreads();
-                {
-                    const int mt = wave >> 1, nt = wave & 1;     // one 32 x 32 tile per wave
-                    f32x16 gkk = {}, gqk = {};
-                    const int ak = (32 * mt + l32) * XS + 8 * hg, aq = (NP + 32 * mt + l32) * XS + 8 * hg;
-                    const int bk = (32 * nt + l32) * XS + 8 * hg;
-#pragma unroll 2
-                    for (int s = 0; s < 8; ++s) {
-                        const bf16x8 a_k = *reinterpret_cast<const bf16x8 *>(Xh + ak + 16 * s);
-                        const bf16x8 a_q = *reinterpret_cast<const bf16x8 *>(Xh + aq + 16 * s);
-                        const bf16x8 b_k = *reinterpret_cast<const bf16x8 *>(Kj + bk + 16 * s);
-                        gkk = mma(a_k, b_k, gkk);
-                        gqk = mma(a_q, b_k, gqk);
-                        if constexpr (F32IN) {
-                            const bf16x8 a_kl = *reinterpret_cast<const bf16x8 *>(Xl + ak + 16 * s);
-                            const bf16x8 a_ql = *reinterpret_cast<const bf16x8 *>(Xl + aq + 16 * s);
-                            const bf16x8 b_kl = *reinterpret_cast<const bf16x8 *>(Kjl + bk + 16 * s);
-                            gkk = mma(a_k, b_kl, gkk);
-                            gkk = mma(a_kl, b_k, gkk);
-                            gqk = mma(a_q, b_kl, gqk);
-                            gqk = mma(a_ql, b_k, gqk);
-                        }
-                    }
-                    const int i = 32 * nt + l32;
-                    const float inv_gi = 1.f / g_all[64 * j + i];   // every node of an earlier chunk is real
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int t = 32 * mt + acc_row(r, hg);
-                        const bool a = (anc_all[(base + t) * MASK_WORDS + j] >> i) & 1ull;
-                        Bm[t * MS + i] = a ? gkk[r] * inv_gi : 0.f;
-                        Am[t * MS + i] = a ? gqk[r] * inv_gi : 0.f;
-                    }
-                }
-                __syncthreads();
-                const rsrc_t ruj = make_rsrc(U + ((size_t)u * u_stride + 64 * j) * D, 64 * D * 4);
-#pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    float ub[8];
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) ub[e] = ld_f32(ruj, ((16 * s + 8 * hg + e) * D + col) * 4);
-                    bf16x8 bh, bl;
-                    split8(ub, bh, bl);
-#pragma unroll
-                    for (int m = 0; m < 2 * MT; ++m) {
-                        const float *crow = (m < MT ? Bm : Am) + (32 * (m % MT) + l32) * MS + 16 * s + 8 * hg;
-                        float c8[8];
-                        *reinterpret_cast<f32x4 *>(c8) = *reinterpret_cast<const f32x4 *>(crow);
-                        *reinterpret_cast<f32x4 *>(c8 + 4) = *reinterpret_cast<const f32x4 *>(crow + 4);
-                        bf16x8 ah, alo;
-                        split8(c8, ah, alo);
-                        accp[m] = mma(ah, bh, accp[m]);
-                        accp[m] = mma(ah, bl, accp[m]);
-                        accp[m] = mma(alo, bh, accp[m]);
-                    }
-                }
-                __syncthreads();                         // the B and A areas and K_j are rewritten next
             }
         }
 
@@ -849,9 +770,9 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || MODE != ONE_PASS) 
         // The A operands (rows of [K; Q] in LDS) are double-buffered one
         // K-step ahead; the scheduling barriers keep the compiler from
         // hoisting every step's operands at once.
-        if constexpr (!XT)
+        f32x16 accp[2 * MT];
 #pragma unroll
-            for (int m = 0; m < 2 * MT; ++m) accp[m] = f32x16{};
+        for (int m = 0; m < 2 * MT; ++m) accp[m] = f32x16{};
         {
             // (one buffer in the fused variant, whose update block needs the registers)
             constexpr int NBUF = FUSE ? 1 : 2;
@@ -911,6 +832,95 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || MODE != ONE_PASS) 
             }
         }
         __syncthreads();
+
+        // ---- tree chunks: coupling to the earlier chunks ------------------
+        // For t in this chunk and i in an earlier chunk j, B[t, i] U_i and
+        // A[t, i] U_i enter eq. 2 through R and O; with B[t, i] =
+        // beta_t (g_t / g_i) k_t . k_i and A[t, i] = (g_t / g_i) q_t . k_i
+        // (i an ancestor of t), both are g_t times
+        //   sum over ancestors i in chunk j of ((x_t . k_i) / g_i) U_i,  x = k or q,
+        // which is added to [K; Q] S0^T before phase 4 scales by g_t (and
+        // beta_t for R).  Per chunk j: the cross gram [K; Q] K_j^T, with
+        // both operands read from the cache in natural d_k order, is masked
+        // and scaled into the K/Q staging area (free once P is done), and its
+        // product with U_j (written by this workgroup one or more chunks ago)
+        // is accumulated on the matrix cores.
+        if constexpr (XT) {
+            float *Ck = reinterpret_cast<float *>(lds), *Cq = Ck + NP * MS;
+            static_assert(2 * NP * MS * 4 <= L::B_OFF, "the coupling blocks fit where K/Q were staged");
+            for (int j = 0; j < chunk; ++j) {            // uniform loop
+                {
+                    const int mt = wave >> 1, nt = wave & 1;  // one 32 x 32 tile of the cross gram per wave
+                    // descriptors bounded to the chunks' rows (uniform), the row in the lane's offset
+                    const size_t row0 = (size_t)u * in_stride;
+                    const rsrc_t rak = make_rsrc(k + (row0 + base) * D, N * Reads::ROW);
+                    const rsrc_t raq = make_rsrc(q + (row0 + base) * D, N * Reads::ROW);
+                    const rsrc_t rbk = make_rsrc(k + (row0 + 64 * j) * D, 64 * Reads::ROW);
+                    const int arow = (32 * mt + l32) * Reads::ROW, brow = (32 * nt + l32) * Reads::ROW;
+                    f32x16 gkk = {}, gqk = {};
+#pragma unroll 2
+                    for (int s = 0; s < 8; ++s) {
+                        const int off = (16 * s + 8 * hg) * (int)sizeof(In);
+                        if constexpr (F32IN) {
+                            float x8[3][8];
+                            bf16x8 h[3], l[3];
+                            const rsrc_t rr[3] = {rak, raq, rbk};
+                            const int ro[3] = {arow, arow, brow};
+#pragma unroll
+                            for (int o3 = 0; o3 < 3; ++o3) {
+                                *reinterpret_cast<f32x4 *>(x8[o3]) = ld_f32x4<CACHED>(rr[o3], ro[o3] + off);
+                                *reinterpret_cast<f32x4 *>(x8[o3] + 4) = ld_f32x4<CACHED>(rr[o3], ro[o3] + off + 16);
+                                split8(x8[o3], h[o3], l[o3]);
+                            }
+                            gkk = mma(h[0], h[2], gkk);
+                            gkk = mma(h[0], l[2], gkk);
+                            gkk = mma(l[0], h[2], gkk);
+                            gqk = mma(h[1], h[2], gqk);
+                            gqk = mma(h[1], l[2], gqk);
+                            gqk = mma(l[1], h[2], gqk);
+                        } else {
+                            const bf16x8 a_k = __builtin_bit_cast(bf16x8, ld_u32x4<CACHED>(rak, arow + off));
+                            const bf16x8 a_q = __builtin_bit_cast(bf16x8, ld_u32x4<CACHED>(raq, arow + off));
+                            const bf16x8 b_k = __builtin_bit_cast(bf16x8, ld_u32x4<CACHED>(rbk, brow + off));
+                            gkk = mma(a_k, b_k, gkk);
+                            gqk = mma(a_q, b_k, gqk);
+                        }
+                    }
+                    const int i = 32 * nt + l32;
+                    const float inv_gi = 1.f / g_all[64 * j + i];   // every node of an earlier chunk is real
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int t = 32 * mt + acc_row(r, hg);
+                        const bool a = (anc_all[(base + t) * MASK_WORDS + j] >> i) & 1ull;
+                        Ck[t * MS + i] = a ? gkk[r] * inv_gi : 0.f;
+                        Cq[t * MS + i] = a ? gqk[r] * inv_gi : 0.f;
+                    }
+                }
+                __syncthreads();
+                const rsrc_t ruj = make_rsrc(U + ((size_t)u * u_stride + 64 * j) * D, 64 * D * 4);
+#pragma unroll
+                for (int s = 0; s < 4; ++s) {
+                    float ub[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) ub[e] = ld_f32(ruj, ((16 * s + 8 * hg + e) * D + col) * 4);
+                    bf16x8 bh, bl;
+                    split8(ub, bh, bl);
+#pragma unroll
+                    for (int m = 0; m < 2 * MT; ++m) {
+                        const float *crow = (m < MT ? Ck : Cq) + (32 * (m % MT) + l32) * MS + 16 * s + 8 * hg;
+                        float c8[8];
+                        *reinterpret_cast<f32x4 *>(c8) = *reinterpret_cast<const f32x4 *>(crow);
+                        *reinterpret_cast<f32x4 *>(c8 + 4) = *reinterpret_cast<const f32x4 *>(crow + 4);
+                        bf16x8 ah, alo;
+                        split8(c8, ah, alo);
+                        accp[m] = mma(ah, bh, accp[m]);
+                        accp[m] = mma(ah, bl, accp[m]);
+                        accp[m] = mma(alo, bh, accp[m]);
+                    }
+                }
+                __syncthreads();                         // the coupling blocks are rewritten next
+            }
+        }
 
         // ---- phase 4: R and g P_Q ---------------------------------------------
 #pragma unroll
@@ -973,7 +983,7 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || MODE != ONE_PASS) 
 #pragma unroll
             for (int it = 0; it < NP * (D / 4) / THREADS; ++it) {
                 const int idx = tid + THREADS * it, t = idx / (D / 4), c = (idx % (D / 4)) * 4;
-                st_u32x4<STREAM>(ru, (t * D + c) * 4, *reinterpret_cast<const uint4 *>(Us + t * US + c));
+                st_u32x4<XT ? CACHED : STREAM>(ru, (t * D + c) * 4, *reinterpret_cast<const uint4 *>(Us + t * US + c));
             }
         }
 #pragma unroll
@@ -1066,6 +1076,7 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || MODE != ONE_PASS) 
         __syncthreads();                                 // LDS is rewritten by the next unit / chunk
         }                                                // chunk
         if constexpr (PRE) {                             // the state after the unit's last token
+            const int lane = threadIdx.x & 63, hg = lane >> 5, col = wave * 32 + (lane & 31);
             const rsrc_t rn = make_rsrc(static_cast<char *>(cm.S_new) + (size_t)u * D * D * SB, D * D * SB);
             const int sbase = (col * D + 4 * hg) * SB;
 #pragma unroll
