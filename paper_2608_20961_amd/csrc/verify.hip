@@ -406,7 +406,7 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || MODE == CHAIN_PREF
             if (wave == 3 && has_next) rd.issue_path(cm, u_next, u_next / H, lane);
             stage_load(0, clen, cp_kv, cp_uv);
         }
-        constexpr bool AHEAD = PRE && !F32IN;            // prefill fetches the next chunk early (bf16 inputs)
+        constexpr bool AHEAD = PRE;                      // the chain prefill fetches the next chunk early
         if (!AHEAD || chunk == 0)                        // (then later chunks were fetched one chunk ahead)
             rd.template issue<XT ? CACHED : STREAM>(S0, q, k, v, alpha, beta, prow, u, N, node0, chunk == 0 || XT,
                                                     tid, lane, wave, hg, col);
@@ -528,7 +528,7 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || MODE == CHAIN_PREF
         __syncthreads();
         // Chain prefill: this chunk's reads are in LDS and registers now, so the
         // next chunk's are issued into the same registers and land during this
-        // chunk's arithmetic (fp32 inputs need twice the registers: not there).
+        // chunk's arithmetic.
         if constexpr (AHEAD) {
             if (chunk + 1 < chunks) {
                 const int N1 = N_all - 64 * (chunk + 1) < 64 ? N_all - 64 * (chunk + 1) : 64;
