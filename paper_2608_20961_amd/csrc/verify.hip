@@ -245,11 +245,12 @@ __device__ __forceinline__ void sweep_column(float (&r)[NP], const float *Bm, in
 // reading S0 again and coupled to the earlier chunks.
 constexpr int ONE_PASS = 0, CHAIN_PREFILL = 1, TREE_CHUNKS = 2;
 
-// Two workgroups per CU where 256 registers per lane suffice.  The chain
-// prefill keeps the state in registers from chunk to chunk, which needs the
-// full register file (one workgroup per CU); so do fp32 inputs at 64 nodes.
+// Two workgroups per CU where 256 registers per lane suffice; fp32 inputs
+// at 64 nodes need the full register file (one workgroup per CU).  The chain
+// prefill keeps the state in registers from chunk to chunk and still runs
+// two workgroups per CU with bf16 inputs.
 template <int NP, bool F32IN, bool FUSE, bool SBF, int MODE>
-__global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || MODE == CHAIN_PREFILL) ? 1 : 2) void verify_kernel(
+__global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_kernel(
     const void *S0, const void *__restrict__ q_, const void *__restrict__ k_,
     const void *__restrict__ v_, const float *__restrict__ alpha, const float *__restrict__ beta,
     const int32_t *__restrict__ parent, int N_all, int in_stride, int u_stride, int H, int units,
@@ -406,7 +407,8 @@ __global__ __launch_bounds__(THREADS, ((F32IN && NP == 64) || MODE == CHAIN_PREF
             if (wave == 3 && has_next) rd.issue_path(cm, u_next, u_next / H, lane);
             stage_load(0, clen, cp_kv, cp_uv);
         }
-        constexpr bool AHEAD = PRE;                      // the chain prefill fetches the next chunk early
+        // (one workgroup per CU only: at two, the other workgroup hides the loads)
+        constexpr bool AHEAD = PRE && F32IN;             // the chain prefill fetches the next chunk early
         if (!AHEAD || chunk == 0)                        // (then later chunks were fetched one chunk ahead)
             rd.template issue<XT ? CACHED : STREAM>(S0, q, k, v, alpha, beta, prow, u, N, node0, chunk == 0 || XT,
                                                     tid, lane, wave, hg, col);
