@@ -397,6 +397,14 @@ def main():
     _, (ms_acc,) = time_steps(torch, [accept], args.steps, args.warmup)
     result["accept_greedy"] = {"avg_launch_ms": round(ms_acc, 5), "sequences": w.B, "nodes": w.N,
                                "mean_accepted": round(float(acc_len.float().mean()), 3)}
+    # What a plain device-to-device copy reaches on this GPU (read + write
+    # bytes): the practical ceiling next to the 8 TB/s vendor peak.
+    src = torch.ones(1 << 28, device="cuda")
+    dst = torch.empty_like(src)
+    _, (ms_copy,) = time_steps(torch, [lambda: dst.copy_(src)], 10, 3)
+    result["hbm_copy_achievable"] = {"GB_per_s": round(2 * 4 * (1 << 28) / (ms_copy * 1e-3) / 1e9, 1),
+                                     "bytes_each_way": 4 * (1 << 28), "avg_launch_ms": round(ms_copy, 5)}
+    del src, dst
     spec = acc.speculative_state_bytes(w)
     result["speculative_state_bytes"] = {"treewy_U": spec["treewy_U"], "treewy_U_k_alpha": spec["treewy_U_k_alpha"],
                                          "snapshot_states": spec["snapshot_states"]}
