@@ -3,7 +3,7 @@
 //    (the accepted node's ancestors and itself, Method eq. 3), one thread per
 //    sequence;
 //  - treewy_accept_greedy: greedy acceptance of the draft tree, one wave per
-//    sequence with lane t holding node t.
+//    sequence with lane t holding nodes t, t + 64, t + 128 and t + 192.
 #include "device.h"
 #include "launch.h"
 

@@ -135,3 +135,51 @@ def test_accept_and_paths(tw, N):
         nodes = wl.ancestors_and_self(parents[b], int(acc[b]))
         assert plen[b].item() == len(nodes)
         assert path[b, :len(nodes)].cpu().tolist() == nodes
+
+
+def test_bad_parent_in_a_later_chunk_counts_as_root(tw):
+    """A parent outside [-1, t-1] in the second chunk is flagged and treated as -1
+    (the header's contract): the outputs equal the oracle's on the repaired tree."""
+    N = 150
+    w = tree_workload(N, 20, B=2, H=2)
+    x = wl.make_inputs(w, seed=11, cfg_key=1800)
+    bad = x["parent"].copy()
+    bad[1, 100] = 120                                  # a later node: invalid
+    bad[1, 140] = -5                                   # below -1: invalid
+    repaired = bad.copy()
+    repaired[1, 100] = repaired[1, 140] = -1
+    x["parent"] = repaired
+    x["path_len"][:] = 0                               # (paths drawn on the original tree)
+    case = Case(w, seed=11, cfg_key=1800, inputs=x)
+    d = case.device()
+    d["parent"] = torch.from_numpy(bad).to(DEV)
+    err = torch.zeros(w.B, dtype=torch.int32, device=DEV)
+    o, U = tw.treewy_verify(d["S0"], d["q"], d["k"], d["v"], d["alpha"], d["beta"], d["parent"], err=err)
+    torch.cuda.synchronize()
+    assert err.tolist() == [0, 1]
+    o_ref, vt_ref, _ = case.oracle()
+    assert_close("o", units_of(o, w, case.check), o_ref, TOL["bf16"])
+    assert_close("U", units_of(U, w, case.check), vt_ref, TOL["bf16"])
+
+
+def test_long_path_broken_deep_inside(tw):
+    """A 200-entry path whose entry 150 skips a node is flagged; the state is kept."""
+    N = 200
+    w = tree_workload(N, N, B=2, H=2, caps=(1,), accept="chain_depth_0_to_N")
+    case = Case(w, seed=12, cfg_key=1900)
+    d = case.device()
+    _, U = tw.treewy_verify(d["S0"], d["q"], d["k"], d["v"], d["alpha"], d["beta"], d["parent"])
+    path = torch.arange(N, dtype=torch.int32, device=DEV).repeat(w.B, 1)
+    path[1, 150:] += 1                                 # 149 -> 151: not a child
+    path[1, N - 1] = -1
+    plen = torch.tensor([N, N - 1], dtype=torch.int32, device=DEV)
+    err = torch.zeros(w.B, dtype=torch.int32, device=DEV)
+    S_new = tw.treewy_commit(d["S0"], U, d["k"], d["alpha"], path, plen, parent=d["parent"], err=err)
+    torch.cuda.synchronize()
+    assert err.tolist() == [0, 2]
+    assert torch.equal(S_new[1], d["S0"][1])
+    S_ref = oracle.commit(case.S0[:w.H], case.unit_view("k")[:w.H], case.unit_view("v")[:w.H],
+                          case.unit_view("alpha")[:w.H], case.unit_view("beta")[:w.H],
+                          np.repeat(case.x["parent"][:1], w.H, axis=0), np.repeat(path[:1].cpu().numpy(), w.H, axis=0),
+                          np.full(w.H, N))
+    assert_close("S_new", units_of(S_new, w, np.arange(w.H)), S_ref, TOL["bf16"])
