@@ -939,6 +939,30 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 accp[m][r] = be_s[t] * (vt - gt * accp[m][r]);
                 accp[MT + m][r] *= gt;
             }
+        // Chain prefill: the Q rows staged in LDS are dead once P is done;
+        // K goes there transposed for the state update at the end of the
+        // chunk: row j holds K[l][d_k = j] (staged at position kperm(j)) in
+        // the contraction order of that update (entry p is node l(p), the
+        // accumulator row order of U), 16-byte chunks swizzled by row.
+        __bf16 *KT = Xh + NP * XS, *KTl = Xl + NP * XS;
+        static_assert(!PRE || D * 64 * 2 <= NP * XS * 2, "K^T fits where Q was staged");
+        auto kt_at = [](int j, int p) { return j * 64 + (((p >> 3) ^ (j & 7)) << 3) + (p & 7); };
+        if constexpr (PRE) {
+            const int j = tid >> 1, p0 = 32 * (tid & 1);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                bf16x8 hi, lo;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int pp = p0 + 8 * c + e, s2 = pp >> 4;
+                    const int l = 32 * (s2 >> 1) + 16 * (s2 & 1) + 8 * (e >> 2) + 4 * ((pp >> 3) & 1) + (e & 3);
+                    hi[e] = Xh[l * XS + Reads::kperm(j)];
+                    if constexpr (F32IN) lo[e] = Xl[l * XS + Reads::kperm(j)];
+                }
+                *reinterpret_cast<bf16x8 *>(KT + kt_at(j, p0 + 8 * c)) = hi;
+                if constexpr (F32IN) *reinterpret_cast<bf16x8 *>(KTl + kt_at(j, p0 + 8 * c)) = lo;
+            }
+        }
         __syncthreads();
 
         // ---- phase 5: U = T R, then O = g P_Q + A U ------------------------
@@ -969,6 +993,9 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             }
             __builtin_amdgcn_sched_barrier(0);
         }
+        // Chain prefill: the update weights g_N / g_l (zero past the chunk)
+        // replace beta, which phase 4 was the last to read.
+        if (PRE && wave == 0) be_s[lane] = lane < N ? g_s[N - 1] / g_s[lane] : 0.f;
         __syncthreads();                                 // every wave is done reading T
         const rsrc_t ru = make_rsrc(PRE ? nullptr : U + (unode0 + base) * D, PRE ? 0 : N * D * 4);
         const rsrc_t ro = make_rsrc(o + node0 * D, N * D * (int)sizeof(In));
@@ -1031,7 +1058,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             //   S <- g_N S + sum_l (g_N / g_l) U_l k_l^T,
             // on the matrix cores as (K^T)(w U) over 32-row blocks of d_k.  The
             // B operand comes straight from the U accumulators (contraction in
-            // their row order), the A operand from K still staged in LDS in
+            // their row order), the A operand from K^T transposed into LDS in
             // the same order; the result rows are this lane's S entries.
             const float gN = g_s[N - 1];
             bf16x8 ubh[2 * MT], ubl[2 * MT];
@@ -1039,28 +1066,27 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             for (int s2 = 0; s2 < 2 * MT; ++s2) {
                 float wu[8];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int l = 32 * (s2 >> 1) + acc_row(8 * (s2 & 1) + e, hg);
-                    wu[e] = l < N ? accv[s2 >> 1][8 * (s2 & 1) + e] * (gN / g_s[l]) : 0.f;
+                for (int e4 = 0; e4 < 8; e4 += 4) {
+                    const int l0 = 32 * (s2 >> 1) + acc_row(8 * (s2 & 1) + e4, hg);   // four consecutive nodes
+                    const f32x4 w4 = *reinterpret_cast<const f32x4 *>(be_s + l0);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) wu[e4 + e] = accv[s2 >> 1][8 * (s2 & 1) + e4 + e] * w4[e];
                 }
                 split8(wu, ubh[s2], ubl[s2]);
             }
 #pragma unroll
             for (int jb = 0; jb < 4; ++jb) {
-                const int kpos = Reads::kperm(32 * jb + l32);
+                const int j = 32 * jb + l32;             // d_k: row l32 of block jb of the update
                 f32x16 d = {};
 #pragma unroll
                 for (int s2 = 0; s2 < 2 * MT; ++s2) {
-                    bf16x8 a, alo;
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const int l = 32 * (s2 >> 1) + acc_row(8 * (s2 & 1) + e, hg);
-                        a[e] = Xh[l * XS + kpos];
-                        if constexpr (F32IN) alo[e] = Xl[l * XS + kpos];
-                    }
+                    const bf16x8 a = *reinterpret_cast<const bf16x8 *>(KT + kt_at(j, 16 * s2 + 8 * hg));
                     d = mma(a, ubh[s2], d);
                     d = mma(a, ubl[s2], d);
-                    if constexpr (F32IN) d = mma(alo, ubh[s2], d);
+                    if constexpr (F32IN) {
+                        const bf16x8 alo = *reinterpret_cast<const bf16x8 *>(KTl + kt_at(j, 16 * s2 + 8 * hg));
+                        d = mma(alo, ubh[s2], d);
+                    }
                 }
 #pragma unroll
                 for (int r = 0; r < 16; r += 4) {
