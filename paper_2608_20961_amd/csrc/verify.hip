@@ -35,7 +35,16 @@
 // Precision.  The matrix cores take bf16; fp32 operands are split into
 // hi + lo bf16 pairs and multiplied in three passes (hi*hi + hi*lo + lo*hi),
 // keeping the products within ~2^-16 of fp32.  bf16 inputs are exact in bf16,
-// so their products with S0 take two passes and the gram one.
+// so their products with S0 take two passes and the gram one; a bf16 state
+// (SBF) is exact too, so P takes one.
+//
+// Variants of the same kernel (template arguments): FUSE commits the
+// previous round's accepted path into S0 on the way in (the fused call) and
+// writes it out as S_new; MODE walks a unit's nodes in 64-node chunks,
+// either as a chain whose state is carried in registers from chunk to chunk
+// and updated at the end of each (the chain prefill), or as a tree of more
+// than 64 nodes, each chunk reading S0 again and coupled to the pseudo-values
+// of its ancestors in earlier chunks before its own solve.
 #include "device.h"
 #include "launch.h"
 
@@ -54,7 +63,6 @@ struct CommitArgs {
     int L_max, N_prev;
     int in_stride;            // rows per unit in k and alpha (N_prev for whole tensors)
     int u_stride;             // rows per unit in U (N_prev for whole tensors)
-    int chain_len;            // >= 0: the path is 0 .. chain_len - 1 of a chain (path arrays unused)
 };
 
 template <int NP, bool F32IN, bool FUSE = false>
@@ -139,12 +147,6 @@ struct UnitReads {
     __device__ __forceinline__ void issue_path(const CommitArgs &cm, int u, int b, int lane) {
         const int np = cm.N_prev;
         cp_al = ld_f32(make_rsrc(cm.alpha + (size_t)u * cm.in_stride, np * 4), lane * 4);
-        if (cm.chain_len >= 0) {                        // the whole chain: node l at entry l
-            cp_len = cm.chain_len;
-            cp_node = lane;
-            cp_par = lane - 1;
-            return;
-        }
         cp_len = ld_i32(make_rsrc(cm.path_len + b, 4), 0);
         cp_node = ld_i32(make_rsrc(cm.path + (size_t)b * cm.L_max, cm.L_max * 4), lane * 4);
         cp_par = cm.parent ? ld_i32(make_rsrc(cm.parent + (size_t)b * np, np * 4), lane * 4) : 0;
@@ -314,8 +316,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         const int par_a = __shfl(rd.cp_par, src);
         const float al_a = __shfl(rd.cp_al, src);
         bool bad = !len_ok;
-        const bool check_parent = cm.parent || cm.chain_len >= 0;
-        if (lane < len) bad = bad || a < 0 || a >= cm.N_prev || a <= pa || (check_parent && par_a != pa);
+        if (lane < len) bad = bad || a < 0 || a >= cm.N_prev || a <= pa || (cm.parent && par_a != pa);
         const bool ok = !__any(bad);
         const int len_c = ok ? len : 0;
         float x = lane < len_c ? al_a : 1.f;
@@ -1193,7 +1194,7 @@ hipError_t launch_commit_verify(const void *S_old, const float *U_prev, const vo
                                 const int32_t *parent, int N, int B, int H, bool f32_in, bool bf16_state,
                                 void *S_new, void *o, float *U, int32_t *err, hipStream_t stream) {
     const CommitArgs cm = {U_prev, k_prev, alpha_prev, path, path_len, parent_prev, S_new, L_max, N_prev,
-                           N_prev, N_prev, -1};
+                           N_prev, N_prev};
     return dispatch<true>(S_old, q, k, v, alpha, beta, parent, N, N, N, B, H, f32_in, bf16_state, o, U, err, cm,
                           stream);
 }
