@@ -143,10 +143,13 @@ def device_inputs(torch, tw, wl, w, seed):
     return x, d
 
 
-def time_steps(torch, launches, steps, warmup):
+def time_steps(torch, launches, steps, warmup, flush=None, stats=None):
     """Run `launches` (a list of callables, one step) W + K times; return the
     average step time and the average time of each launch (HIP events on the
-    stream the kernels run on)."""
+    stream the kernels run on).  With `flush`, it runs between steps (outside
+    every launch's events) and the step time is the sum of the launch times.
+    With `stats` (a list), the p10 / p50 / p90 of each launch's times are
+    appended to it."""
     for _ in range(warmup):
         for f in launches:
             f()
@@ -158,14 +161,19 @@ def time_steps(torch, launches, steps, warmup):
     torch.cuda.synchronize()
     t0.record(stream)
     for i in range(steps):
+        if flush is not None:
+            flush()
         ev[i][0].record(stream)
         for j, f in enumerate(launches):
             f()
             ev[i][j + 1].record(stream)
     t1.record(stream)
     torch.cuda.synchronize()
-    total = t0.elapsed_time(t1) / steps
-    per = [float(np.mean([ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(steps)])) for j in range(len(launches))]
+    times = [[ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(steps)] for j in range(len(launches))]
+    per = [float(np.mean(t)) for t in times]
+    total = sum(per) if flush is not None else t0.elapsed_time(t1) / steps
+    if stats is not None:
+        stats.extend([round(float(x), 5) for x in np.percentile(t, (10, 50, 90))] for t in times)
     return total, per
 
 
@@ -251,7 +259,15 @@ def main():
         tw.treewy_commit(S0_commit, U, d["k"], d["alpha"], d["path"], d["path_len"], parent=d["parent"],
                          S_new=S_new)
 
-    ms_step, (ms_verify, ms_commit) = time_steps(torch, [verify, commit], args.steps, args.warmup)
+    # A workload whose step fits in the 256 MiB last-level cache would be
+    # served from it step after step: then 512 MiB are written between steps
+    # (outside the timed launches).
+    flush = None
+    if acc.verify_bytes(w) + acc.commit_bytes(w, x["path_len"]) < (1 << 30):
+        scratch = torch.empty(1 << 27, device="cuda")
+        flush = scratch.zero_
+    dist = []
+    ms_step, (ms_verify, ms_commit) = time_steps(torch, [verify, commit], args.steps, args.warmup, flush, dist)
     log("timed %d steps: %.4f ms/step (verify %.4f, commit %.4f)" % (args.steps, ms_step, ms_verify, ms_commit))
     src_hash = kernel_source_hash()
     vb = acc.verify_bytes(w)
@@ -270,12 +286,13 @@ def main():
         "dtype": w.in_dtype, "data": "synthetic",
         "config": {"workload": w.describe(), "B": w.B, "H": w.H, "N": w.N, "d_k": w.d_k, "d_v": w.d_v,
                    "step": "treewy_verify + treewy_commit (out of place)", "accumulate": "f32",
-                   "state": "f32", "parallelism": "none (1 GPU)"},
+                   "state": "f32", "parallelism": "none (1 GPU)",
+                   "cache_flushed_between_steps": flush is not None},
         "roofline": dict(dominant, kernel="treewy_verify" if dominant is rf_verify else "treewy_commit"),
-        "verify": dict(rf_verify, nodes_per_s=round(nodes / (ms_verify * 1e-3), 1),
+        "verify": dict(rf_verify, launch_ms_p10_p50_p90=dist[0], nodes_per_s=round(nodes / (ms_verify * 1e-3), 1),
                        head_nodes_per_s=round(w.units * w.N / (ms_verify * 1e-3), 1),
                        useful_tflops=round(acc.verify_flops(w) / (ms_verify * 1e-3) / 1e12, 2)),
-        "commit": dict(rf_commit, pct_hbm_peak=round(100 * rf_commit["frac"], 2)),
+        "commit": dict(rf_commit, launch_ms_p10_p50_p90=dist[1], pct_hbm_peak=round(100 * rf_commit["frac"], 2)),
         "kernel_source_hash": src_hash,
     }
     # Fused: the previous round's commit inside this round's verify
