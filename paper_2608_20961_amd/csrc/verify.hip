@@ -203,41 +203,28 @@ struct UnitReads {
     }
 };
 
-// One column of the dense sweep that builds row t of T = (I + B)^{-1} (see
-// phase 3a), then the next column down.  Compile-time recursion keeps every
-// index into r static (r stays in registers).  Each column's row read must
-// not be hoisted far ahead (that needs a register per element of B); two
-// fences do it, whichever the compiler schedules without spilling for this
-// size: for 32 nodes the row address passes through an empty asm that also
-// takes the previous column's pivot (rows are fetched one column ahead), for
-// 64 a compiler memory barrier closes each column.
-template <int I, int NP, int MS>
-__device__ __forceinline__ void sweep_column(float (&r)[NP], const float *Bm, int t, float prev) {
+// One column of the dense sweep that builds row t of a 32-row block of
+// T = (I + B)^{-1} (see phase 3a), then the next column down.  Compile-time
+// recursion keeps every index into r static (r stays in registers).  A
+// column's row read must not be hoisted far ahead (that needs a register per
+// element of B): its address passes through an empty asm that also takes the
+// previous column's pivot, so rows are fetched one column ahead.
+template <int I, int MS>
+__device__ __forceinline__ void sweep_column(float (&r)[32], const float *Bm, int t, float prev) {
     if constexpr (I >= 0) {
         const float x = I < t ? -r[I] : 0.f;            // T[t, I] (zero on and above the diagonal)
         r[I] = x;
-        if constexpr (NP <= 32) {
-            int base = I * MS;
-            asm volatile("" : "+v"(base) : "v"(prev));
-            f32x4 bi[(I + 3) / 4 > 0 ? (I + 3) / 4 : 1];
+        int base = I * MS;
+        asm volatile("" : "+v"(base) : "v"(prev));
+        f32x4 bi[(I + 3) / 4 > 0 ? (I + 3) / 4 : 1];
 #pragma unroll
-            for (int c = 0; c < (I + 3) / 4; ++c) bi[c] = *reinterpret_cast<const f32x4 *>(Bm + base + 4 * c);
+        for (int c = 0; c < (I + 3) / 4; ++c) bi[c] = *reinterpret_cast<const f32x4 *>(Bm + base + 4 * c);
 #pragma unroll
-            for (int c = 0; c < (I + 3) / 4; ++c)
+        for (int c = 0; c < (I + 3) / 4; ++c)
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    if (4 * c + e < I) r[4 * c + e] = fmaf(x, bi[c][e], r[4 * c + e]);
-        } else {
-#pragma unroll
-            for (int c = 0; c < (I + 3) / 4; ++c) {
-                const f32x4 bi = *reinterpret_cast<const f32x4 *>(Bm + I * MS + 4 * c);
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    if (4 * c + e < I) r[4 * c + e] = fmaf(x, bi[e], r[4 * c + e]);
-            }
-            asm volatile("" ::: "memory");
-        }
-        sweep_column<I - 1, NP, MS>(r, Bm, t, x);
+            for (int e = 0; e < 4; ++e)
+                if (4 * c + e < I) r[4 * c + e] = fmaf(x, bi[c][e], r[4 * c + e]);
+        sweep_column<I - 1, MS>(r, Bm, t, x);
     }
 }
 
@@ -730,7 +717,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 #pragma unroll
                 for (int e = 0; e < 4; ++e) r[4 * c + e] = bt[e];
             }
-            sweep_column<31, 32, MS>(r, Bblk, tl, 0.f);
+            sweep_column<31, MS>(r, Bblk, tl, 0.f);
             if (NP == 64 || lane < 32) {
                 float *Tt = Bm + (off + tl) * MS + off;
 #pragma unroll
