@@ -178,8 +178,10 @@ def pin_brute_force_small_trees(orc, d=6, seed=4):
     assert count == 1 * 1 + 2 * 2 + 6 * 3 + 24 * 4
 
 
-def pin_closed_form(orc, cases=((0, 2, 1, 4), (2, 2, 2, 16), (3, 1, 2, 64), (4, 2, 1, 32)), tol=1e-12):
-    """Oracle == the paper's closed form (eq. 2 solve, read-out, eq. 3)."""
+def pin_closed_form(orc, cases=((0, 2, 1, 4), (2, 2, 2, 16), (3, 1, 2, 64), (4, 2, 1, 32), (3, 1, 1, 200),
+                                (1, 1, 1, 150)), tol=1e-12):
+    """Oracle == the paper's closed form (eq. 2 solve, read-out, eq. 3), up to
+    trees and chains past one 64-node chunk."""
     for cfg, B, H, N in cases:
         w = wl.scaled(wl.WORKLOADS[cfg], B=B, H=H, N=N)
         x = wl.make_inputs(w, seed=11)

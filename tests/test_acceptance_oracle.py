@@ -70,8 +70,8 @@ def _characterise(parent, draft, target, root, path, bonus):
 def test_random_trees_satisfy_the_characterisation(seed):
     from paper_2608_20961_amd import workload as wl
     rng = np.random.default_rng(seed)
-    n = int(rng.integers(1, 65))
-    parent = [int(p) for p in wl.random_tree(rng, n, int(rng.integers(1, min(n, 9) + 1)), (64,))]
+    n = int(rng.integers(1, 65)) if seed % 2 else int(rng.integers(65, 257))
+    parent = [int(p) for p in wl.random_tree(rng, n, int(rng.integers(1, min(n, 40) + 1)), (256,))]
     vocab = int(rng.integers(1, 5))
     draft = [int(x) for x in rng.integers(0, vocab, n)]
     target = [int(x) for x in rng.integers(0, vocab, n)]
