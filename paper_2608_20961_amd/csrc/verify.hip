@@ -21,8 +21,10 @@
 // dense column sweep for deep ones).  U = T R
 // and A U then run on the matrix cores with R and U taken straight from the
 // accumulator registers (the contraction index is permuted to match the
-// accumulator layout; T and A are read in the same permuted order).  U and O
-// leave through LDS as whole-row 16-byte stores.
+// accumulator layout; T and A are read in the same permuted order).  U
+// leaves straight from its accumulators (each store instruction writes whole
+// 128-byte lines) at 64 nodes, else through LDS; bf16 O through LDS as
+// whole-row 16-byte stores.
 //
 // Streaming.  All of a unit's HBM reads are issued at once, in the order they
 // are consumed (tree and gates, K/Q, V, then S0), through buffer descriptors
@@ -984,19 +986,27 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // Chain prefill: the update weights g_N / g_l (zero past the chunk)
         // replace beta, which phase 4 was the last to read.
         if (PRE && wave == 0) be_s[lane] = lane < N ? g_s[N - 1] / g_s[lane] : 0.f;
-        __syncthreads();                                 // every wave is done reading T
         const rsrc_t ru = make_rsrc(PRE ? nullptr : U + (unode0 + base) * D, PRE ? 0 : N * D * 4);
         const rsrc_t ro = make_rsrc(o + node0 * D, N * D * (int)sizeof(In));
-        if constexpr (!PRE) {                            // (the chain prefill keeps U in registers and K in LDS)
+        // U leaves while A U runs (rows of padding nodes fall past the end of
+        // the descriptor and are dropped).  At 64 nodes in one pass, straight
+        // from the accumulators: each store instruction writes the lane
+        // group's 32 columns, one whole 128-byte line, of two rows.  Otherwise
+        // (where those registers are not to spare) through LDS as whole rows,
+        // 16 bytes per lane.
+        constexpr bool U_DIRECT = MODE == ONE_PASS && NP == 64;
+        if constexpr (U_DIRECT) {
+#pragma unroll
+            for (int m = 0; m < MT; ++m)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    st_f32<STREAM>(ru, ((32 * m + acc_row(r, hg)) * D + col) * 4, accv[m][r]);
+        } else if constexpr (!PRE) {                     // (the chain prefill keeps U in registers and K in LDS)
 #pragma unroll
             for (int m = 0; m < MT; ++m)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) Us[(32 * m + acc_row(r, hg)) * US + col] = accv[m][r];
-        }
-        __syncthreads();
-        // U leaves as whole rows, 16 bytes per lane (rows of padding nodes fall
-        // past the end of the descriptor and are dropped) while A U runs.
-        if constexpr (!PRE) {
+            __syncthreads();
 #pragma unroll
             for (int it = 0; it < NP * (D / 4) / THREADS; ++it) {
                 const int idx = tid + THREADS * it, t = idx / (D / 4), c = (idx % (D / 4)) * 4;
@@ -1024,6 +1034,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             __builtin_amdgcn_sched_barrier(0);
         }
         if constexpr (!F32IN) {
+            __syncthreads();                             // o is staged over T: every wave is done with U = T R
 #pragma unroll
             for (int m = 0; m < MT; ++m)
 #pragma unroll
@@ -1048,6 +1059,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             // B operand comes straight from the U accumulators (contraction in
             // their row order), the A operand from K^T transposed into LDS in
             // the same order; the result rows are this lane's S entries.
+            if constexpr (F32IN) __syncthreads();          // the weights (bf16 inputs: ordered by the o staging)
             const float gN = g_s[N - 1];
             bf16x8 ubh[2 * MT], ubl[2 * MT];
 #pragma unroll
