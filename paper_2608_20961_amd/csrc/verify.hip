@@ -953,7 +953,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 if constexpr (F32IN) *reinterpret_cast<bf16x8 *>(KTl + kt_at(j, p0 + 8 * c)) = lo;
             }
         }
-        __syncthreads();
+        // (no barrier: phase 4 works in registers; T was written before the
+        // barrier that ends P, and the K^T writes above are read after later ones)
 
         // ---- phase 5: U = T R, then O = g P_Q + A U ------------------------
         // K-step s covers nodes [16s, 16s+16) in the order the accumulator
