@@ -48,12 +48,12 @@ __global__ __launch_bounds__(THREADS) void path_from_node_kernel(
 // whose draft token equals the target's prediction at the current position
 // (lowest index among equal siblings) until no child matches.  Children have
 // larger indices than their parent, so the walk ends within N steps.
+template <int W>                                        // nodes per lane: lane + 64 w, w < W
 __global__ __launch_bounds__(THREADS) void accept_greedy_kernel(
     const int32_t *__restrict__ parent, const int32_t *__restrict__ draft,
     const int32_t *__restrict__ target, const int32_t *__restrict__ root, int N, int B, int L_max,
     int32_t *__restrict__ path, int32_t *__restrict__ path_len, int32_t *__restrict__ bonus,
     int32_t *__restrict__ err) {
-    constexpr int W = MAX_TREE / 64;                     // nodes per lane: lane + 64 w
     const int lane = threadIdx.x & 63;
     const int b = blockIdx.x * (THREADS / 64) + (threadIdx.x >> 6);
     if (b >= B) return;                                  // whole waves leave together
@@ -102,6 +102,7 @@ __global__ __launch_bounds__(THREADS) void accept_greedy_kernel(
         const int l = lane + 64 * w;
         if (l < L_max) path[(size_t)b * L_max + l] = fits && l < len ? mine[w] : -1;
     }
+    for (int l = 64 * W + lane; l < L_max; l += 64) path[(size_t)b * L_max + l] = -1;   // past every node
     if (lane == 0) {
         path_len[b] = fits ? len : 0;
         if (bonus) bonus[b] = want;
@@ -113,8 +114,13 @@ hipError_t launch_accept_greedy(const int32_t *parent, const int32_t *draft, con
                                 int32_t *path_len, int32_t *bonus, int32_t *err, hipStream_t stream) {
     const int per_block = THREADS / 64;
     const int blocks = (B + per_block - 1) / per_block;
-    hipLaunchKernelGGL(accept_greedy_kernel, dim3((unsigned)blocks), dim3(THREADS), 0, stream, parent,
-                       draft, target, root, N, B, L_max, path, path_len, bonus, err);
+#define TREEWY_ACCEPT(W)                                                                                      \
+    hipLaunchKernelGGL((accept_greedy_kernel<W>), dim3((unsigned)blocks), dim3(THREADS), 0, stream, parent,   \
+                       draft, target, root, N, B, L_max, path, path_len, bonus, err)
+    if (N <= 64) TREEWY_ACCEPT(1);
+    else if (N <= 128) TREEWY_ACCEPT(2);
+    else TREEWY_ACCEPT(MAX_TREE / 64);
+#undef TREEWY_ACCEPT
     return hipGetLastError();
 }
 

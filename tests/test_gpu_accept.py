@@ -111,3 +111,12 @@ def test_accepted_paths_feed_the_fused_commit(tw):
     assert_close("S_new", units_of(S_new, w, units), S_ref, tol)
     assert_close("o", units_of(o, w, units), o_ref, tol)
     assert_close("U", units_of(Un, w, units), vt_ref, tol)
+
+
+def test_path_longer_than_the_tree(tw):
+    """L_max above N (and above one word of nodes): entries past the path are -1."""
+    rng = np.random.default_rng(77)
+    for N, L_max in ((40, 130), (100, 256)):
+        parents = np.stack([wl.random_tree(rng, N, int(rng.integers(1, N + 1)), (N,)) for _ in range(8)])
+        tok = wl.acceptance_tokens(parents, seed=N, vocab=2, plant=True)
+        check(tw, parents, tok, L_max, "N=%d L_max=%d" % (N, L_max))
