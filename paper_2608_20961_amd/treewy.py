@@ -88,6 +88,9 @@ def _need(t: torch.Tensor, name: str, dtype, shape) -> None:
         raise TypeError("%s must be a torch.Tensor" % name)
     if t.device.type != "cuda":
         raise ValueError("%s must be on a GPU" % name)
+    if t.device.index is not None and t.device.index != torch.cuda.current_device():
+        raise ValueError("%s is on %s but the current device is cuda:%d (kernels launch on the current device)"
+                         % (name, t.device, torch.cuda.current_device()))
     if t.dtype != dtype:
         raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
     if tuple(t.shape) != tuple(shape):
