@@ -23,7 +23,8 @@
 // accumulator registers (the contraction index is permuted to match the
 // accumulator layout; T and A are read in the same permuted order).  U
 // leaves straight from its accumulators (each store instruction writes whole
-// 128-byte lines) at 64 nodes, else through LDS; bf16 O through LDS as
+// 128-byte lines) at 64 nodes, else through LDS; so does bf16 O in plain
+// verify at 64 nodes (half lines, merged in L2), else through LDS as
 // whole-row 16-byte stores.
 //
 // Streaming.  All of a unit's HBM reads are issued at once, in the order they
@@ -1034,7 +1035,19 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             }
             __builtin_amdgcn_sched_barrier(0);
         }
-        if constexpr (!F32IN) {
+        // Plain verify at 64 nodes: bf16 o straight from the accumulators as
+        // well.  A store instruction writes half a line (32 bf16) of two rows;
+        // the default policy lets L2 merge the halves from neighbouring waves.
+        // (The fused kernel keeps the staging: it has no registers to spare.)
+        constexpr bool O_DIRECT = U_DIRECT && !FUSE;
+        if constexpr (O_DIRECT && !F32IN) {
+#pragma unroll
+            for (int m = 0; m < MT; ++m)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, (__bf16)accp[MT + m][r]), ro,
+                                                          ((32 * m + acc_row(r, hg)) * D + col) * 2, 0, CACHED);
+        } else if constexpr (!F32IN) {
             __syncthreads();                             // o is staged over T: every wave is done with U = T R
 #pragma unroll
             for (int m = 0; m < MT; ++m)
