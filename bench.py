@@ -184,6 +184,16 @@ def roofline(bytes_per_launch, ms, traffic):
             "algorithmic_bytes": int(bytes_per_launch), "avg_launch_ms": round(ms, 5)}
 
 
+def _cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, wl, x, seed, target_s):
     """The float64 oracle (verify + commit) on a bounded sample of units.
 
@@ -220,6 +230,7 @@ def cpu_baseline(w, wl, x, seed, target_s):
     dt = run(units, warm(units))
     nodes_per_s = (len(units) / H) * N / dt       # a sequence's N nodes cost H units of work
     return {"value": round(nodes_per_s, 1), "unit": "nodes/s", "cores": orc.threads(), "kind": "oracle",
+            "cpu_model": _cpu_model(), "host_cpus": os.cpu_count(),
             "sample": "%d of %d (sequence, head) units of the same workload; float64 verify + commit "
                       "took %.2f s; nodes/s = units/H * N / time" % (len(units), w.units, dt)}
 
