@@ -3,7 +3,8 @@
 // with g_a the product of alpha along the path and w_l = g_a / g_{path_l} the
 // product of alpha over the path nodes after path_l.
 //
-// One workgroup per (sequence, head) streams its state: every thread owns
+// A workgroup streams one (sequence, head) state at a time (fp32 states: the
+// resident workgroups walk the units; bf16 states: one unit each): every thread owns
 // sixteen 16-byte chunks at stride 4 KiB (an fp32 state: 4 entries each; a
 // bf16 state: 8 entries, read and written in eight chunks), so each load and
 // store instruction of the workgroup covers 4 KiB of contiguous HBM.  A bf16
@@ -25,7 +26,7 @@ __global__ __launch_bounds__(THREADS) void commit_kernel(
     const void *S0, const float *__restrict__ U, const void *__restrict__ k_,
     const float *__restrict__ alpha, const int32_t *__restrict__ path,
     const int32_t *__restrict__ path_len, int L_max, const int32_t *__restrict__ parent, int N,
-    int H, void *S_new, int32_t *__restrict__ err) {
+    int H, void *S_new, int32_t *__restrict__ err, int units) {
     constexpr int SB = SBF ? 2 : 4;                      // bytes per state entry
     constexpr int CH = 16 / SB;                          // entries per 16-byte chunk
     constexpr int NCH = D * D / CH / THREADS;            // chunks per thread
@@ -38,7 +39,9 @@ __global__ __launch_bounds__(THREADS) void commit_kernel(
     __shared__ int s_bad;
 
     const In *k = static_cast<const In *>(k_);
-    const int tid = threadIdx.x, u = blockIdx.x, b = u / H;
+    const int tid = threadIdx.x;
+    for (int u = blockIdx.x; u < units; u += gridDim.x) {   // resident workgroups walk the units
+    const int b = u / H;
     const size_t node0 = (size_t)u * N;
 
     // The state is touched once: stream it past the caches on the way in and out.
@@ -152,17 +155,36 @@ __global__ __launch_bounds__(THREADS) void commit_kernel(
         }
         st_u32x4<STREAM>(rd, (tid + THREADS * i) * 16, out);
     }
+    if constexpr (SBF) break;                            // a bf16 state: one unit per workgroup (see the launch)
+    __syncthreads();                                     // the shared path data is rewritten by the next unit
+    }                                                    // unit
 }
 
 hipError_t launch_commit(const void *S0, const float *U, const void *k, const float *alpha,
                          const int32_t *path, const int32_t *path_len, int L_max,
                          const int32_t *parent, int N, int B, int H, bool f32_k, bool bf16_state,
                          void *S_new, int32_t *err, hipStream_t stream) {
-    const dim3 grid((unsigned)(B * H)), block(THREADS);
+    const int units = B * H;
     const size_t lds = (size_t)2 * (L_max < STAGE_ROWS ? L_max : STAGE_ROWS) * D * sizeof(float);
+    // fp32 state: a grid of resident workgroups (as many as fit on the GPU),
+    // each walking units, so a workgroup starts the next unit's state reads as
+    // soon as it is done.  A bf16 state (half the bytes per unit) runs faster
+    // with one workgroup per unit.
+    auto grid_of = [&](const void *kern) {
+        if (bf16_state) return dim3((unsigned)units);
+        int dev = 0, cus = 256, per_cu = 1;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+            cus = 256;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, THREADS, lds) != hipSuccess || per_cu < 1)
+            per_cu = 1;
+        const long long g = (long long)cus * per_cu;
+        return dim3((unsigned)(units < g ? units : g));
+    };
 #define TREEWY_COMMIT(F, S)                                                                                   \
-    hipLaunchKernelGGL((commit_kernel<F, S>), grid, block, lds, stream, S0, U, k, alpha, path, path_len, L_max, \
-                       parent, N, H, S_new, err)
+    hipLaunchKernelGGL((commit_kernel<F, S>), grid_of(reinterpret_cast<const void *>(&commit_kernel<F, S>)),    \
+                       dim3(THREADS), lds, stream, S0, U, k, alpha, path, path_len, L_max, parent, N, H, S_new, err, \
+                       units)
     if (f32_k) {
         if (bf16_state) TREEWY_COMMIT(true, true);
         else TREEWY_COMMIT(true, false);
