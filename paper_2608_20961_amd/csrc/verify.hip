@@ -1035,11 +1035,12 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             }
             __builtin_amdgcn_sched_barrier(0);
         }
-        // Plain verify at 64 nodes: bf16 o straight from the accumulators as
-        // well.  A store instruction writes half a line (32 bf16) of two rows;
-        // the default policy lets L2 merge the halves from neighbouring waves.
-        // (The fused kernel keeps the staging: it has no registers to spare.)
-        constexpr bool O_DIRECT = U_DIRECT && !FUSE;
+        // At 64 nodes, bf16 o straight from the accumulators as well.  A store
+        // instruction writes half a line (32 bf16) of two rows; the default
+        // policy lets L2 merge the halves from neighbouring waves.  (The fused
+        // kernel with an fp32 state keeps the staging: it has no registers to
+        // spare.)
+        constexpr bool O_DIRECT = U_DIRECT && (!FUSE || SBF);
         if constexpr (O_DIRECT && !F32IN) {
 #pragma unroll
             for (int m = 0; m < MT; ++m)
