@@ -183,3 +183,10 @@ def test_long_path_broken_deep_inside(tw):
                           np.repeat(case.x["parent"][:1], w.H, axis=0), np.repeat(path[:1].cpu().numpy(), w.H, axis=0),
                           np.full(w.H, N))
     assert_close("S_new", units_of(S_new, w, np.arange(w.H)), S_ref, TOL["bf16"])
+
+
+def test_fp32_inputs_many_units_per_workgroup(tw):
+    """fp32 inputs run one workgroup per CU: 1024 units make each workgroup walk
+    several units (the per-unit ancestor tables in LDS are rebuilt each time)."""
+    w = tree_workload(100, 12, "f32", B=16, H=64)
+    check(tw, Case(w, seed=13, cfg_key=2000, check_units=wl.sample_units(w, 10)), "f32 tree N=100, 1024 units")
