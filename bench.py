@@ -238,8 +238,8 @@ def cpu_baseline(w, wl, x, seed, target_s):
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py runs on exactly one GPU: the verify/commit path has no cross-GPU step "
-              "and this build measures one GPU's share (got --gpus %d)" % args.gpus, file=sys.stderr)
+        print("bench.py runs on exactly one GPU: the verify/commit path has no cross-GPU step, "
+              "and it measures one GPU's share (got --gpus %d)" % args.gpus, file=sys.stderr)
         sys.exit(2)
     import torch
     if args.copy_calibration:

@@ -29,8 +29,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libtreewy.so")
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError("libtreewy.so is not built; run `python -m paper_2608_20961_amd.build` "
-                      "(or __graft_entry__.build()) first")
+    raise ImportError("libtreewy.so is not built; run `python -m paper_2608_20961_amd.build` first")
 
 lib = ctypes.CDLL(LIB_PATH)
 
