@@ -150,9 +150,14 @@ struct UnitReads {
     __device__ __forceinline__ void issue_path(const CommitArgs &cm, int u, int b, int lane) {
         const int np = cm.N_prev;
         cp_al = ld_f32(make_rsrc(cm.alpha + (size_t)u * cm.in_stride, np * 4), lane * 4);
-        cp_len = ld_i32(make_rsrc(cm.path_len + b, 4), 0);
+        // (an opaque zero offset: a uniform load's result would be moved to a
+        // scalar register at once, which waits for it before the unit's own reads)
+        cp_len = ld_i32(make_rsrc(cm.path_len + b, 4), opaque(0));
         cp_node = ld_i32(make_rsrc(cm.path + (size_t)b * cm.L_max, cm.L_max * 4), lane * 4);
-        cp_par = cm.parent ? ld_i32(make_rsrc(cm.parent + (size_t)b * np, np * 4), lane * 4) : 0;
+        // (without a parent array the descriptor is empty and the read gives 0:
+        // no branch, so nothing here waits for these reads)
+        const int32_t *pp = cm.parent;
+        cp_par = ld_i32(make_rsrc(pp ? pp + (size_t)b * np : nullptr, pp ? np * 4 : 0), lane * 4);
     }
 
     // Every HBM read of unit u, in the order the unit consumes them.
@@ -172,7 +177,10 @@ struct UnitReads {
                                           int u, int N, size_t node0, bool load_state, int tid,
                                           int lane, int wave, int hg, int col) {
         if (wave == 0) {                                // prow: this unit's parents of the N nodes (null: a chain)
-            par = prow ? ld_i32(make_rsrc(prow, N * 4), lane * 4) : lane - 1;
+            // (read unconditionally, an empty descriptor giving 0 for a chain,
+            // whose parents the walk takes as lane - 1: a branch here would
+            // make the compiler wait for every outstanding memory operation)
+            par = ld_i32(make_rsrc(prow, prow ? N * 4 : 0), lane * 4);
             al = ld_f32(make_rsrc(alpha + node0, N * 4), lane * 4);
             be = ld_f32(make_rsrc(beta + node0, N * 4), lane * 4);
         }
@@ -414,7 +422,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // decay and ancestors (g_all, anc_all), so the lane takes them over
         // at once; ext holds the ancestor words of the earlier chunks.
         if (wave == 0) {
-            int ptr = lane < N ? rd.par : -1;
+            int ptr = lane < N ? (parent ? rd.par : lane - 1) : -1;   // (no parent array: a chain)
             if (lane < N && (ptr < -1 || ptr >= base + lane)) {
                 flag_error(err, b, TREEWY_FLAG_BAD_PARENT);
                 ptr = -1;
