@@ -841,11 +841,12 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // (i an ancestor of t), both are g_t times
         //   sum over ancestors i in chunk j of ((x_t . k_i) / g_i) U_i,  x = k or q,
         // which is added to [K; Q] S0^T before phase 4 scales by g_t (and
-        // beta_t for R).  Per chunk j: the cross gram [K; Q] K_j^T, with
-        // both operands read from the cache in natural d_k order, is masked
+        // beta_t for R).  Per chunk j: the cross gram [K; Q] K_j^T is masked
         // and scaled into the K/Q staging area (free once P is done), and its
         // product with U_j (written by this workgroup one or more chunks ago)
-        // is accumulated on the matrix cores.
+        // is accumulated on the matrix cores.  The chunk's own K and Q come
+        // from that staging area for the first earlier chunk and from the
+        // cache after it has been overwritten; K_j always from the cache.
         if constexpr (XT) {
             float *Ck = reinterpret_cast<float *>(lds), *Cq = Ck + NP * MS;
             static_assert(2 * NP * MS * 4 <= L::B_OFF, "the coupling blocks fit where K/Q were staged");
@@ -859,6 +860,40 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                     const rsrc_t rbk = make_rsrc(k + (row0 + 64 * j) * D, 64 * Reads::ROW);
                     const int arow = (32 * mt + l32) * Reads::ROW, brow = (32 * nt + l32) * Reads::ROW;
                     f32x16 gkk = {}, gqk = {};
+                    if (j == 0) {
+                        // This chunk's K and Q are still staged in LDS (in the
+                        // kperm order of d_k): read them there, and the rows of
+                        // chunk 0 in the same order, element e of step s being
+                        // d_k = 16 s + 8 (e / 4) + 4 hg + e % 4.
+                        const __bf16 *xk = Xh + (32 * mt + l32) * XS + 8 * hg, *xq = xk + NP * XS;
+#pragma unroll 2
+                        for (int s = 0; s < 8; ++s) {
+                            const int o0 = (16 * s + 4 * hg) * (int)sizeof(In), o1 = o0 + 8 * (int)sizeof(In);
+                            const bf16x8 ah_k = *reinterpret_cast<const bf16x8 *>(xk + 16 * s);
+                            const bf16x8 ah_q = *reinterpret_cast<const bf16x8 *>(xq + 16 * s);
+                            if constexpr (F32IN) {
+                                const bf16x8 al_k = *reinterpret_cast<const bf16x8 *>(xk + 16 * s + (Xl - Xh));
+                                const bf16x8 al_q = *reinterpret_cast<const bf16x8 *>(xq + 16 * s + (Xl - Xh));
+                                float x8[8];
+                                *reinterpret_cast<f32x4 *>(x8) = ld_f32x4<CACHED>(rbk, brow + o0);
+                                *reinterpret_cast<f32x4 *>(x8 + 4) = ld_f32x4<CACHED>(rbk, brow + o1);
+                                bf16x8 bh, bl;
+                                split8(x8, bh, bl);
+                                gkk = mma(ah_k, bh, gkk);
+                                gkk = mma(ah_k, bl, gkk);
+                                gkk = mma(al_k, bh, gkk);
+                                gqk = mma(ah_q, bh, gqk);
+                                gqk = mma(ah_q, bl, gqk);
+                                gqk = mma(al_q, bh, gqk);
+                            } else {
+                                const uint2 b0 = ld_u32x2<CACHED>(rbk, brow + o0), b1 = ld_u32x2<CACHED>(rbk, brow + o1);
+                                const bf16x8 b_k = __builtin_bit_cast(bf16x8, make_uint4(b0.x, b0.y, b1.x, b1.y));
+                                gkk = mma(ah_k, b_k, gkk);
+                                gqk = mma(ah_q, b_k, gqk);
+                            }
+                        }
+                        __syncthreads();                 // the coupling blocks are written over the staged K/Q
+                    } else {
 #pragma unroll 2
                     for (int s = 0; s < 8; ++s) {
                         const int off = (16 * s + 8 * hg) * (int)sizeof(In);
@@ -886,6 +921,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                             gkk = mma(a_k, b_k, gkk);
                             gqk = mma(a_q, b_k, gqk);
                         }
+                    }
                     }
                     const int i = 32 * nt + l32;
                     const float inv_gi = 1.f / g_all[64 * j + i];   // every node of an earlier chunk is real
