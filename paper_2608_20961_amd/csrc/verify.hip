@@ -866,7 +866,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                         // chunk 0 in the same order, element e of step s being
                         // d_k = 16 s + 8 (e / 4) + 4 hg + e % 4.
                         const __bf16 *xk = Xh + (32 * mt + l32) * XS + 8 * hg, *xq = xk + NP * XS;
-#pragma unroll 2
+                        constexpr int XU = SBF ? 2 : 4;  // steps in flight (a bf16 state has fewer registers to spare)
+#pragma unroll XU
                         for (int s = 0; s < 8; ++s) {
                             const int o0 = (16 * s + 4 * hg) * (int)sizeof(In), o1 = o0 + 8 * (int)sizeof(In);
                             const bf16x8 ah_k = *reinterpret_cast<const bf16x8 *>(xk + 16 * s);
