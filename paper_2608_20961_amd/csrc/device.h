@@ -96,6 +96,31 @@ template <int P = CACHED> __device__ __forceinline__ void st_f32(rsrc_t r, int o
     __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned int, x), r, off, 0, P);
 }
 
+// One butterfly step of quad_transpose: lanes with `bit` clear exchange x[q]
+// with x[p] of the lane `bit` away (DPP quad permutation CTRL).
+template <int BIT, int CTRL>
+__device__ __forceinline__ void quad_swap(f32x4 &xp, f32x4 &xq, int lane) {
+    const bool hi = lane & BIT;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {                       // (value selects: a select of references goes through memory)
+        const float a = xp[e], b = xq[e];
+        const float got =
+            __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, hi ? a : b), CTRL, 0xF, 0xF, false));
+        xp[e] = hi ? got : a;
+        xq[e] = hi ? b : got;
+    }
+}
+
+// 4 x 4 transpose across the four lanes of each quad: afterwards lane i of a
+// quad holds in x[r] what lane r held in x[i].  Two butterfly steps, each
+// swapping one bit of the lane index with the same bit of the register index.
+__device__ __forceinline__ void quad_transpose(f32x4 (&x)[4], int lane) {
+    quad_swap<1, 0xB1>(x[0], x[1], lane);               // quad_perm [1, 0, 3, 2]
+    quad_swap<1, 0xB1>(x[2], x[3], lane);
+    quad_swap<2, 0x4E>(x[0], x[2], lane);               // quad_perm [2, 3, 0, 1]
+    quad_swap<2, 0x4E>(x[1], x[3], lane);
+}
+
 // A copy of x the compiler cannot see through (keeps derived values inside a loop).
 __device__ __forceinline__ int opaque(int x) {
     asm volatile("" : "+v"(x));

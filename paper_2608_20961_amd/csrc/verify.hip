@@ -34,6 +34,8 @@
 // and U/o stores cover whole cache lines per instruction and go out
 // non-temporal; S0's operand-layout loads reach each line through four
 // instructions and keep the default policy so the line stays in L2 between them.
+// The fused call's fp32 S_new leaves in whole lines too, after a transpose
+// across each quad of lanes (a bf16 S_new keeps the operand layout).
 //
 // Precision.  The matrix cores take bf16; fp32 operands are split into
 // hi + lo bf16 pairs and multiplied in three passes (hi*hi + hi*lo + lo*hi),
@@ -794,7 +796,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                     load_a(0, s);
                 else if (s < 7)
                     load_a((s + 1) & 1, s + 1);
-                if constexpr (FUSE) {                    // S0 pieces of step s: commit update, then S_new
+                if constexpr (FUSE) {                    // S0 pieces of step s: commit update, then (bf16) S_new
                     if (upd_in_p) {
                         if ((s & 1) == 0) dcur = rank_block(s >> 1, f32x16{});
 #pragma unroll
@@ -805,12 +807,9 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                             rd.sset(s, h, x);                   // a bf16 state is rounded here, then used
                         }
                     }
+                    if constexpr (SBF) {
 #pragma unroll
-                    for (int h = 0; h < 2; ++h) {
-                        if constexpr (SBF)
-                            st_u32x2<CACHED>(rn, sbase + 32 * s + 16 * h, rd.s0[s][h]);
-                        else
-                            st_u32x4<CACHED>(rn, sbase + 64 * s + 32 * h, __builtin_bit_cast(uint4, rd.s0[s][h]));
+                        for (int h = 0; h < 2; ++h) st_u32x2<CACHED>(rn, sbase + 32 * s + 16 * h, rd.s0[s][h]);
                     }
                 }
                 bf16x8 bh, bl;
@@ -828,6 +827,20 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                     accp[m] = mma(afr[s % NBUF][m], bh, accp[m]);
                     if constexpr (!SBF) accp[m] = mma(afr[s % NBUF][m], bl, accp[m]);
                     if constexpr (F32IN) accp[m] = mma(alo[s % NBUF][m], bh, accp[m]);
+                }
+                // fp32 S_new in whole 128-byte lines: after steps 2L and 2L+1,
+                // the four lanes of a quad hold line L of four rows, two
+                // 16-byte pieces per row and lane group each.  A transpose
+                // across the quad gives each store instruction one row per
+                // quad, so that it writes eight whole lines.
+                if constexpr (FUSE && !SBF) {
+                    if (s & 1) {
+                        f32x4 x4[4] = {rd.s0[s - 1][0], rd.s0[s - 1][1], rd.s0[s][0], rd.s0[s][1]};
+                        quad_transpose(x4, lane);
+                        const int off = ((wave * 32 + (l32 & ~3)) * D + 32 * (s >> 1) + 8 * (l32 & 3) + 4 * hg) * 4;
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) st_u32x4<STREAM>(rn, off + r * D * 4, __builtin_bit_cast(uint4, x4[r]));
+                    }
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
