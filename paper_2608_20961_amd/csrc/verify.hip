@@ -34,8 +34,8 @@
 // and U/o stores cover whole cache lines per instruction and go out
 // non-temporal; S0's operand-layout loads reach each line through four
 // instructions and keep the default policy so the line stays in L2 between them.
-// The fused call's fp32 S_new leaves in whole lines too, after a transpose
-// across each quad of lanes (a bf16 S_new keeps the operand layout).
+// The state written back (the fused call's S_new, the chain prefill's S_T)
+// leaves in whole lines too, after a transpose across each quad of lanes.
 //
 // Precision.  The matrix cores take bf16; fp32 operands are split into
 // hi + lo bf16 pairs and multiplied in three passes (hi*hi + hi*lo + lo*hi),
@@ -198,6 +198,39 @@ struct UnitReads {
 #pragma unroll
         for (int i = 0; i < VQN; ++i) vq[i] = ld_u32x4<STREAM>(rv, (tid + THREADS * i) * 16);
         if (load_state) issue_state(S0, u, hg, col);    // (chain prefill: the state is already in registers)
+    }
+
+    // Writes line L (128 bytes) of each of this wave's 32 state rows to rn in
+    // whole lines: the steps s of line L (two for fp32, four for bf16) hold
+    // it as 16- or 8-byte pieces spread over the lanes of each quad and the
+    // two lane groups.  A bf16 state first swaps pieces across the lane
+    // groups so that lane group hg holds the 16-byte pieces of h = hg; then
+    // a 4 x 4 transpose across each quad gives store instruction r row r of
+    // every quad: eight whole lines per instruction, non-temporal.  The
+    // registers read are left unchanged.
+    static constexpr int LINE_STEPS = SBF ? 4 : 2;
+    __device__ __forceinline__ void store_state_line(rsrc_t rn, int L, int wave, int lane) const {
+        const int l32 = lane & 31, hg = lane >> 5;
+        f32x4 x4[4];
+        if constexpr (SBF) {
+#pragma unroll
+            for (int sp = 0; sp < 4; ++sp) {
+                const uint2 a = s0[4 * L + sp][0], c = s0[4 * L + sp][1];
+                const auto rx = __builtin_amdgcn_permlane32_swap(a.x, c.x, false, false);
+                const auto ry = __builtin_amdgcn_permlane32_swap(a.y, c.y, false, false);
+                x4[sp] = __builtin_bit_cast(f32x4, make_uint4(rx[0], ry[0], rx[1], ry[1]));
+            }
+        } else {
+            x4[0] = s0[2 * L][0];
+            x4[1] = s0[2 * L][1];
+            x4[2] = s0[2 * L + 1][0];
+            x4[3] = s0[2 * L + 1][1];
+        }
+        quad_transpose(x4, lane);
+        constexpr int PER16 = 16 / SB;                  // state entries per 16-byte piece
+        const int off = ((wave * 32 + (l32 & ~3)) * D + 8 * PER16 * L + 2 * PER16 * (l32 & 3) + PER16 * hg) * SB;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) st_u32x4<STREAM>(rn, off + r * D * SB, __builtin_bit_cast(uint4, x4[r]));
     }
 
     __device__ __forceinline__ void issue_state(const void *S0, int u, int hg, int col) {
@@ -665,7 +698,6 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         }
         const rsrc_t rn = make_rsrc(FUSE ? static_cast<char *>(cm.S_new) + (size_t)u * D * D * SB : nullptr,
                                     FUSE ? D * D * SB : 0);
-        const int sbase = (col * D + 4 * hg) * SB;
         const bool shallow = *shallow_s != 0;
         // ---- phase 3a: rows of T = (I + B)^{-1}, on wave 3 while the others start on P
         // (T (I + B))[t, j] = 0 for j != t gives, walking t's ancestors j from
@@ -796,7 +828,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                     load_a(0, s);
                 else if (s < 7)
                     load_a((s + 1) & 1, s + 1);
-                if constexpr (FUSE) {                    // S0 pieces of step s: commit update, then (bf16) S_new
+                if constexpr (FUSE) {                    // S0 pieces of step s: commit update
                     if (upd_in_p) {
                         if ((s & 1) == 0) dcur = rank_block(s >> 1, f32x16{});
 #pragma unroll
@@ -806,10 +838,6 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                             for (int i = 0; i < 4; ++i) x[i] = fmaf(ga, x[i], dcur[8 * (s & 1) + 4 * h + i]);
                             rd.sset(s, h, x);                   // a bf16 state is rounded here, then used
                         }
-                    }
-                    if constexpr (SBF) {
-#pragma unroll
-                        for (int h = 0; h < 2; ++h) st_u32x2<CACHED>(rn, sbase + 32 * s + 16 * h, rd.s0[s][h]);
                     }
                 }
                 bf16x8 bh, bl;
@@ -828,19 +856,9 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                     if constexpr (!SBF) accp[m] = mma(afr[s % NBUF][m], bl, accp[m]);
                     if constexpr (F32IN) accp[m] = mma(alo[s % NBUF][m], bh, accp[m]);
                 }
-                // fp32 S_new in whole 128-byte lines: after steps 2L and 2L+1,
-                // the four lanes of a quad hold line L of four rows, two
-                // 16-byte pieces per row and lane group each.  A transpose
-                // across the quad gives each store instruction one row per
-                // quad, so that it writes eight whole lines.
-                if constexpr (FUSE && !SBF) {
-                    if (s & 1) {
-                        f32x4 x4[4] = {rd.s0[s - 1][0], rd.s0[s - 1][1], rd.s0[s][0], rd.s0[s][1]};
-                        quad_transpose(x4, lane);
-                        const int off = ((wave * 32 + (l32 & ~3)) * D + 32 * (s >> 1) + 8 * (l32 & 3) + 4 * hg) * 4;
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) st_u32x4<STREAM>(rn, off + r * D * 4, __builtin_bit_cast(uint4, x4[r]));
-                    }
+                // S_new leaves line by line once the steps that hold a line are done.
+                if constexpr (FUSE) {
+                    if (s % Reads::LINE_STEPS == Reads::LINE_STEPS - 1) rd.store_state_line(rn, s / Reads::LINE_STEPS, wave, lane);
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -1177,18 +1195,10 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         __syncthreads();                                 // LDS is rewritten by the next unit / chunk
         }                                                // chunk
         if constexpr (PRE) {                             // the state after the unit's last token
-            const int lane = threadIdx.x & 63, hg = lane >> 5, col = wave * 32 + (lane & 31);
+            const int lane = threadIdx.x & 63;
             const rsrc_t rn = make_rsrc(static_cast<char *>(cm.S_new) + (size_t)u * D * D * SB, D * D * SB);
-            const int sbase = (col * D + 4 * hg) * SB;
 #pragma unroll
-            for (int s2 = 0; s2 < 8; ++s2)
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    if constexpr (SBF)
-                        st_u32x2<STREAM>(rn, sbase + 32 * s2 + 16 * h, rd.s0[s2][h]);
-                    else
-                        st_u32x4<STREAM>(rn, sbase + 64 * s2 + 32 * h, __builtin_bit_cast(uint4, rd.s0[s2][h]));
-                }
+            for (int L = 0; L < 8 / Reads::LINE_STEPS; ++L) rd.store_state_line(rn, L, wave, lane);
         }
     }
 }
