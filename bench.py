@@ -42,7 +42,9 @@ def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=10)
+    # (the first few dozen launches of a section run while the GPU's clocks
+    # settle under the sustained HBM load; 30 untimed steps cover that)
+    p.add_argument("--warmup", type=int, default=30)
     p.add_argument("--workload", type=int, default=3)
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-snapshot", action="store_true")
