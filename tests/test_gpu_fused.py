@@ -232,3 +232,31 @@ def test_fused_empty_current_draft(tw):
                           np.repeat(case.xp["parent"], H, axis=0), np.repeat(case.xp["path"], H, axis=0),
                           np.repeat(case.xp["path_len"], H, axis=0))
     assert_close("N=0 S_new", units_of(S_new, w, case.check), S_ref, TOL["bf16"])
+
+
+@pytest.mark.parametrize("state", ["f32", "bf16"])
+@pytest.mark.parametrize("N", [16, 64])
+def test_fused_in_place_bit_identical(tw, state, N):
+    """S_new written over S_old gives bit for bit what the out-of-place call
+    gives (each state row is read by the wave that writes it, before any of
+    its lines is written), and the out-of-place call leaves S_old alone.
+    Both state types and both padded node counts (32 and 64)."""
+    w = wl.Workload("fused", 3, 4, N, 128, 128, "bf16", "tree", min(N, 8), (4, 4, 2), (0.85, 0.999),
+                    (0.05, 0.95), 16, "uniform_node")
+    say("[gpu] fused in place: %s state, N=%d" % (state, N))
+    case = TwoRounds(w, w, seed=70 + N)
+    dp, dc = _dev(case.xp, w), _dev(case.xc, w)
+    sdt = torch.float32 if state == "f32" else torch.bfloat16
+    S_old = torch.from_numpy(case.S_old.reshape(w.B, w.H, 128, 128)).to(DEV).to(sdt)
+    _, U_prev = tw.treewy_verify(S_old, dp["q"], dp["k"], dp["v"], dp["alpha"], dp["beta"], dp["parent"])
+    args = (U_prev, dp["k"], dp["alpha"], dp["path"], dp["path_len"], dc["q"], dc["k"], dc["v"], dc["alpha"],
+            dc["beta"], dc["parent"])
+    keep = S_old.clone()
+    S_out, o_out, U_out = tw.treewy_commit_verify(S_old, *args, parent_prev=dp["parent"])
+    torch.cuda.synchronize()
+    assert torch.equal(S_old, keep)
+    S_in = S_old.clone()
+    S_ret, o_in, U_in = tw.treewy_commit_verify(S_in, *args, parent_prev=dp["parent"], S_new=S_in)
+    torch.cuda.synchronize()
+    assert S_ret.data_ptr() == S_in.data_ptr()
+    assert torch.equal(S_in, S_out) and torch.equal(o_in, o_out) and torch.equal(U_in, U_out)
