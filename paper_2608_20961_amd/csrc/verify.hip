@@ -23,9 +23,9 @@
 // accumulator registers (the contraction index is permuted to match the
 // accumulator layout; T and A are read in the same permuted order).  U
 // leaves straight from its accumulators (each store instruction writes whole
-// 128-byte lines) at 64 nodes, else through LDS; so does bf16 O in plain
-// verify at 64 nodes (half lines, merged in L2), else through LDS as
-// whole-row 16-byte stores.
+// 128-byte lines) at 64 nodes in one pass, else through LDS; so does bf16 O
+// at 64 nodes in one pass, except in the fused call with an fp32 state (half
+// lines, merged in L2), else through LDS as whole-row 16-byte stores.
 //
 // Streaming.  All of a unit's HBM reads are issued at once, in the order they
 // are consumed (tree and gates, K/Q, V, then S0), through buffer descriptors
