@@ -882,6 +882,18 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             float *Ck = reinterpret_cast<float *>(lds), *Cq = Ck + NP * MS;
             static_assert(2 * NP * MS * 4 <= L::B_OFF, "the coupling blocks fit where K/Q were staged");
             for (int j = 0; j < chunk; ++j) {            // uniform loop
+                // This wave's columns of U_j, for the product: with an fp32
+                // state issued before the barriers, so that they arrive during
+                // them (a bf16 state has no registers to spare for that).
+                constexpr bool EARLY_U = !SBF;
+                float ub[4][8];
+                auto load_u = [&]() {
+                    const rsrc_t ruj = make_rsrc(U + ((size_t)u * u_stride + 64 * j) * D, 64 * D * 4);
+#pragma unroll
+                    for (int s = 0; s < 4; ++s)
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) ub[s][e] = ld_f32(ruj, ((16 * s + 8 * hg + e) * D + col) * 4);
+                };
                 {
                     const int mt = wave >> 1, nt = wave & 1;  // one 32 x 32 tile of the cross gram per wave
                     // descriptors bounded to the chunks' rows (uniform), the row in the lane's offset
@@ -924,7 +936,6 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                                 gqk = mma(ah_q, b_k, gqk);
                             }
                         }
-                        __syncthreads();                 // the coupling blocks are written over the staged K/Q
                     } else {
 #pragma unroll 2
                     for (int s = 0; s < 8; ++s) {
@@ -955,6 +966,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                         }
                     }
                     }
+                    if constexpr (EARLY_U) load_u();
+                    if (j == 0) __syncthreads();         // the coupling blocks are written over the staged K/Q
                     const int i = 32 * nt + l32;
                     const float inv_gi = 1.f / g_all[64 * j + i];   // every node of an earlier chunk is real
 #pragma unroll
@@ -966,14 +979,11 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                     }
                 }
                 __syncthreads();
-                const rsrc_t ruj = make_rsrc(U + ((size_t)u * u_stride + 64 * j) * D, 64 * D * 4);
+                if constexpr (!EARLY_U) load_u();
 #pragma unroll
                 for (int s = 0; s < 4; ++s) {
-                    float ub[8];
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) ub[e] = ld_f32(ruj, ((16 * s + 8 * hg + e) * D + col) * 4);
                     bf16x8 bh, bl;
-                    split8(ub, bh, bl);
+                    split8(ub[s], bh, bl);
 #pragma unroll
                     for (int m = 0; m < 2 * MT; ++m) {
                         const float *crow = (m < MT ? Ck : Cq) + (32 * (m % MT) + l32) * MS + 16 * s + 8 * hg;
