@@ -1141,9 +1141,13 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 #pragma unroll
                 for (int r = 0; r < 16; ++r) Os[(32 * m + acc_row(r, hg)) * OS + col] = (__bf16)accp[MT + m][r];
             __syncthreads();
+            // (chain prefill: an opaque copy of tid.  These offsets repeat the
+            // staging's row / column split, and the compiler would otherwise
+            // keep those values live across the whole chunk, spilled.)
+            const int tid_o = PRE ? opaque(tid) : tid;
 #pragma unroll
             for (int it = 0; it < NP * (D / 8) / THREADS; ++it) {
-                const int idx = tid + THREADS * it, t = idx / (D / 8), c = (idx % (D / 8)) * 8;
+                const int idx = tid_o + THREADS * it, t = idx / (D / 8), c = (idx % (D / 8)) * 8;
                 st_u32x4<STREAM>(ro, (t * D + c) * 2, *reinterpret_cast<const uint4 *>(Os + t * OS + c));
             }
         } else {
