@@ -385,10 +385,11 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         for (int chunk = 0; chunk < chunks; ++chunk) {
         // Lane indices are re-derived each pass from an opaque copy so the
         // per-lane offsets below are recomputed here instead of being hoisted
-        // out of the loops and held in registers for their whole length.
-        const int tid = opaque(threadIdx.x), lane = tid & 63;
-        const int l32 = lane & 31, hg = lane >> 5;
-        const int col = wave * 32 + l32;                 // this lane's d_v column (= row of S0)
+        // out of the loops and held in registers for their whole length (the
+        // chain prefill re-derives them again before phase 5).
+        int tid = opaque(threadIdx.x), lane = tid & 63;
+        int l32 = lane & 31, hg = lane >> 5;
+        int col = wave * 32 + l32;                       // this lane's d_v column (= row of S0)
         const int N = MODE != ONE_PASS ? (N_all - 64 * chunk < 64 ? N_all - 64 * chunk : 64) : N_all;
         const int base = XT ? 64 * chunk : 0;            // tree index of this chunk's node 0
         const int32_t *prow = parent ? parent + (size_t)b * N_all + base : nullptr;
@@ -1043,6 +1044,16 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // (no barrier: phase 4 works in registers; T was written before the
         // barrier that ends P, and the K^T writes above are read after later ones)
 
+        // Chain prefill: lane indices re-derived once more for the chunk's
+        // second half, so that offsets formed from them in the first half are
+        // not held (spilled) across the solve.
+        if constexpr (PRE) {
+            tid = opaque(threadIdx.x);
+            lane = tid & 63;
+            l32 = lane & 31;
+            hg = lane >> 5;
+            col = wave * 32 + l32;
+        }
         // ---- phase 5: U = T R, then O = g P_Q + A U ------------------------
         // K-step s covers nodes [16s, 16s+16) in the order the accumulator
         // holds them: slot e of lane group hg is node 32(s/2) + 16(s%2) +
