@@ -116,8 +116,9 @@ struct VerifyLds {
 
 // One unit's HBM reads, held in registers from issue to use.  Every read goes
 // through a buffer descriptor bounded to this unit's rows, so rows of padding
-// nodes (t >= N) read as zero.
-template <int NP, bool F32IN, bool FUSE = false, bool SBF = false>
+// nodes (t >= N) read as zero.  CHAIN: the nodes form a chain (the chain
+// prefill), so there is no parent array to read.
+template <int NP, bool F32IN, bool FUSE = false, bool SBF = false, bool CHAIN = false>
 struct UnitReads {
     using In = typename std::conditional<F32IN, float, __bf16>::type;
     static constexpr int MT = NP / 32;
@@ -181,8 +182,9 @@ struct UnitReads {
         if (wave == 0) {                                // prow: this unit's parents of the N nodes (null: a chain)
             // (read unconditionally, an empty descriptor giving 0 for a chain,
             // whose parents the walk takes as lane - 1: a branch here would
-            // make the compiler wait for every outstanding memory operation)
-            par = ld_i32(make_rsrc(prow, prow ? N * 4 : 0), lane * 4);
+            // make the compiler wait for every outstanding memory operation.
+            // The chain prefill (CHAIN) has no parent array and reads none.)
+            if constexpr (!CHAIN) par = ld_i32(make_rsrc(prow, prow ? N * 4 : 0), lane * 4);
             al = ld_f32(make_rsrc(alpha + node0, N * 4), lane * 4);
             be = ld_f32(make_rsrc(beta + node0, N * 4), lane * 4);
         }
@@ -295,7 +297,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
     constexpr bool PRE = MODE == CHAIN_PREFILL, XT = MODE == TREE_CHUNKS;
     static_assert(!(MODE != ONE_PASS && (FUSE || NP != 64)), "chunked modes run 64-node chunks, unfused");
     using L = VerifyLds<NP, F32IN, FUSE>;
-    using Reads = UnitReads<NP, F32IN, FUSE, SBF>;
+    using Reads = UnitReads<NP, F32IN, FUSE, SBF, PRE>;
     constexpr int SB = Reads::SB;
     constexpr int MT = NP / 32;                          // 32-row tiles of nodes
     constexpr int XS = L::XS, MS = L::MS, US = L::US, OS = L::OS;
@@ -458,7 +460,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // decay and ancestors (g_all, anc_all), so the lane takes them over
         // at once; ext holds the ancestor words of the earlier chunks.
         if (wave == 0) {
-            int ptr = lane < N ? (parent ? rd.par : lane - 1) : -1;   // (no parent array: a chain)
+            int ptr = lane < N ? ((!PRE && parent) ? rd.par : lane - 1) : -1;   // (no parent array: a chain)
             if (lane < N && (ptr < -1 || ptr >= base + lane)) {
                 flag_error(err, b, TREEWY_FLAG_BAD_PARENT);
                 ptr = -1;
