@@ -387,8 +387,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         for (int chunk = 0; chunk < chunks; ++chunk) {
         // Lane indices are re-derived each pass from an opaque copy so the
         // per-lane offsets below are recomputed here instead of being hoisted
-        // out of the loops and held in registers for their whole length (the
-        // chunked modes re-derive them again before phase 5).
+        // out of the loops and held in registers for their whole length (they
+        // are re-derived again before phase 5).
         int tid = opaque(threadIdx.x), lane = tid & 63;
         int l32 = lane & 31, hg = lane >> 5;
         int col = wave * 32 + l32;                       // this lane's d_v column (= row of S0)
@@ -1046,10 +1046,10 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // (no barrier: phase 4 works in registers; T was written before the
         // barrier that ends P, and the K^T writes above are read after later ones)
 
-        // Chunked modes: lane indices re-derived once more for the chunk's
-        // second half, so that offsets formed from them in the first half are
-        // not held (spilled) across the solve and the coupling.
-        if constexpr (PRE || XT) {
+        // Lane indices re-derived once more for the second half of the pass,
+        // so that offsets formed from them in the first half are not held in
+        // registers (or spilled) across P, the solve and the coupling.
+        {
             tid = opaque(threadIdx.x);
             lane = tid & 63;
             l32 = lane & 31;
