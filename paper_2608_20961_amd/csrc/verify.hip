@@ -24,8 +24,8 @@
 // accumulator layout; T and A are read in the same permuted order).  U
 // leaves straight from its accumulators (each store instruction writes whole
 // 128-byte lines) at 64 nodes in one pass, else through LDS; so does bf16 O
-// at 64 nodes in one pass, except in the fused call with an fp32 state (half
-// lines, merged in L2), else through LDS as whole-row 16-byte stores.
+// at 64 nodes in one pass (half lines, merged in L2), else through LDS as
+// whole-row 16-byte stores.
 //
 // Streaming.  All of a unit's HBM reads are issued at once, in the order they
 // are consumed (tree and gates, K/Q, V, then S0), through buffer descriptors
@@ -1136,10 +1136,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         }
         // At 64 nodes, bf16 o straight from the accumulators as well.  A store
         // instruction writes half a line (32 bf16) of two rows; the default
-        // policy lets L2 merge the halves from neighbouring waves.  (The fused
-        // kernel with an fp32 state keeps the staging: it has no registers to
-        // spare.)
-        constexpr bool O_DIRECT = U_DIRECT && (!FUSE || SBF);
+        // policy lets L2 merge the halves from neighbouring waves.
+        constexpr bool O_DIRECT = U_DIRECT;
         if constexpr (O_DIRECT && !F32IN) {
 #pragma unroll
             for (int m = 0; m < MT; ++m)
