@@ -885,10 +885,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             float *Ck = reinterpret_cast<float *>(lds), *Cq = Ck + NP * MS;
             static_assert(2 * NP * MS * 4 <= L::B_OFF, "the coupling blocks fit where K/Q were staged");
             for (int j = 0; j < chunk; ++j) {            // uniform loop
-                // This wave's columns of U_j, for the product: with an fp32
-                // state issued before the barriers, so that they arrive during
-                // them (a bf16 state has no registers to spare for that).
-                constexpr bool EARLY_U = !SBF;
+                // This wave's columns of U_j, for the product, issued before
+                // the barriers so that they arrive during them.
                 float ub[4][8];
                 auto load_u = [&]() {
                     const rsrc_t ruj = make_rsrc(U + ((size_t)u * u_stride + 64 * j) * D, 64 * D * 4);
@@ -969,7 +967,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                         }
                     }
                     }
-                    if constexpr (EARLY_U) load_u();
+                    load_u();
                     if (j == 0) __syncthreads();         // the coupling blocks are written over the staged K/Q
                     const int i = 32 * nt + l32;
                     const float inv_gi = 1.f / g_all[64 * j + i];   // every node of an earlier chunk is real
@@ -982,7 +980,6 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                     }
                 }
                 __syncthreads();
-                if constexpr (!EARLY_U) load_u();
 #pragma unroll
                 for (int s = 0; s < 4; ++s) {
                     bf16x8 bh, bl;
