@@ -1081,9 +1081,12 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             }
             __builtin_amdgcn_sched_barrier(0);
         }
-        // Chain prefill: the update weights g_N / g_l (zero past the chunk)
-        // replace beta, which phase 4 was the last to read.
-        if (PRE && wave == 0) be_s[lane] = lane < N ? g_s[N - 1] / g_s[lane] : 0.f;
+        // Chain prefill: the update weights g_N / g_l (zero past the chunk),
+        // written where the ancestor masks were: those were last read before
+        // the barrier that ends P, whereas beta is still read by the other
+        // waves' phase 4 (no barrier orders this write after those reads).
+        float *wt_s = reinterpret_cast<float *>(anc_s);
+        if (PRE && wave == 0) wt_s[lane] = lane < N ? g_s[N - 1] / g_s[lane] : 0.f;
         const rsrc_t ru = make_rsrc(PRE ? nullptr : U + (unode0 + base) * D, PRE ? 0 : N * D * 4);
         const rsrc_t ro = make_rsrc(o + node0 * D, N * D * (int)sizeof(In));
         // U leaves while A U runs (rows of padding nodes fall past the end of
@@ -1181,7 +1184,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 #pragma unroll
                 for (int e4 = 0; e4 < 8; e4 += 4) {
                     const int l0 = 32 * (s2 >> 1) + acc_row(8 * (s2 & 1) + e4, hg);   // four consecutive nodes
-                    const f32x4 w4 = *reinterpret_cast<const f32x4 *>(be_s + l0);
+                    const f32x4 w4 = *reinterpret_cast<const f32x4 *>(wt_s + l0);
 #pragma unroll
                     for (int e = 0; e < 4; ++e) wu[e4 + e] = accv[s2 >> 1][8 * (s2 & 1) + e4 + e] * w4[e];
                 }
