@@ -24,8 +24,8 @@
 // accumulator layout; T and A are read in the same permuted order).  U
 // leaves straight from its accumulators (each store instruction writes whole
 // 128-byte lines) at 64 nodes in one pass, else through LDS; so does bf16 O
-// at 64 nodes in one pass (half lines, merged in L2), else through LDS as
-// whole-row 16-byte stores.
+// at 64 nodes in one pass and in the chain prefill (half lines, merged in
+// L2), else through LDS as whole-row 16-byte stores.
 //
 // Streaming.  All of a unit's HBM reads are issued at once, in the order they
 // are consumed (tree and gates, K/Q, V, then S0), through buffer descriptors
@@ -1134,10 +1134,11 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             }
             __builtin_amdgcn_sched_barrier(0);
         }
-        // At 64 nodes, bf16 o straight from the accumulators as well.  A store
-        // instruction writes half a line (32 bf16) of two rows; the default
-        // policy lets L2 merge the halves from neighbouring waves.
-        constexpr bool O_DIRECT = U_DIRECT;
+        // At 64 nodes and in the chain prefill, bf16 o straight from the
+        // accumulators as well.  A store instruction writes half a line (32
+        // bf16) of two rows; the default policy lets L2 merge the halves from
+        // neighbouring waves (rows of padding nodes fall past the descriptor).
+        constexpr bool O_DIRECT = U_DIRECT || PRE;
         if constexpr (O_DIRECT && !F32IN) {
 #pragma unroll
             for (int m = 0; m < MT; ++m)
@@ -1175,7 +1176,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             // B operand comes straight from the U accumulators (contraction in
             // their row order), the A operand from K^T transposed into LDS in
             // the same order; the result rows are this lane's S entries.
-            if constexpr (F32IN) __syncthreads();          // the weights (bf16 inputs: ordered by the o staging)
+            __syncthreads();                             // the weights and K^T, from every wave
             const float gN = g_s[N - 1];
             bf16x8 ubh[2 * MT], ubl[2 * MT];
 #pragma unroll
