@@ -755,8 +755,9 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // so that one accumulator tile is live at a time).  LDS accesses of
         // one wave complete in order, so no barrier separates the steps.
         if (!shallow && wave == 3) {
-            // (the solve is the critical path here: its wave goes first at
-            // instruction issue on its SIMD, then back to normal)
+            // (the solve, then this wave's share of P, is the critical path
+            // here: the wave goes first at instruction issue on its SIMD until
+            // P is done)
             __builtin_amdgcn_s_setprio(2);
             const int tl = lane & 31;                                // row within a diagonal block
             const int off = NP == 64 ? 32 * (lane >> 5) : 0;
@@ -805,7 +806,6 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 #pragma unroll
                 for (int r = 0; r < 16; ++r) B10[acc_row(r, hg) * MS + l32] = -tt[r];
             }
-            __builtin_amdgcn_s_setprio(0);
         }
 
         // ---- phase 3: P = [K; Q] S0^T for this wave's 32 columns ----------
@@ -870,6 +870,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
+        __builtin_amdgcn_s_setprio(0);                  // (wave 3 after a deep solve)
         __syncthreads();
 
         // ---- tree chunks: coupling to the earlier chunks ------------------
