@@ -169,3 +169,21 @@ def test_binding_raises_with_status(tw):
     with pytest.raises(tw.TreewyError) as e:
         tw._check(tw.TREEWY_ERR_UNSUPPORTED, "treewy_verify")
     assert e.value.status == tw.TREEWY_ERR_UNSUPPORTED and "unsupported" in str(e.value)
+
+
+def test_binding_refuses_without_library(tmp_path):
+    """The binding has no fallback: a copy of it next to no libtreewy.so
+    raises ImportError on import."""
+    import shutil
+    import subprocess
+    import sys
+    src = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_2608_20961_amd",
+                       "treewy.py")
+    pkg = tmp_path / "nolib"
+    pkg.mkdir()
+    (pkg / "__init__.py").write_text("")
+    shutil.copy(src, pkg / "treewy.py")
+    r = subprocess.run([sys.executable, "-c", "import nolib.treewy"], cwd=str(tmp_path), capture_output=True,
+                       text=True, timeout=300)
+    assert r.returncode != 0
+    assert "ImportError" in r.stderr and "not built" in r.stderr
