@@ -122,6 +122,12 @@ def test_fused_full_size_397B_tree(tw):
     TwoRounds(w, w, seed=20, check_units=wl.sample_units(w, 24)).check_against_oracle(tw, "c3 full")
 
 
+def test_fused_full_size_stress_tree(tw):
+    """The 32-node stress workload at full size (16384 units), 24 sampled."""
+    w = wl.WORKLOADS[4]
+    TwoRounds(w, w, seed=21, check_units=wl.sample_units(w, 24)).check_against_oracle(tw, "c4 full")
+
+
 @pytest.mark.parametrize("Np,Nc", [(16, 64), (64, 8), (5, 33), (64, 64)])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_fused_round_sizes_differ(tw, Np, Nc, dtype):
