@@ -125,3 +125,29 @@ def test_prefill_many_units_per_workgroup(tw):
     es = assert_close("S_T", S_T.float().cpu().numpy().reshape(w.units, 128, 128)[units], S_ref, TOL["bf16"])
     eo = assert_close("o", o.float().cpu().numpy().reshape(w.units, T, 128)[units], o_ref, TOL["bf16"])
     say("[gpu] prefill over %d units: max rel err S_T %.2e o %.2e" % (w.units, es, eo))
+
+
+def test_prefill_bench_length(tw):
+    """The benchmark's chunk count: T = 1024 (sixteen 64-token chunks), 512
+    units, bf16 tokens and an fp32 state; sampled units against the oracle."""
+    T, B, H = 1024, 8, 64
+    w = wl.Workload("prefill", B, H, T, 128, 128, "bf16", "chain", T, (1,), (0.85, 0.999), (0.05, 0.95), 16,
+                    "chain_depth_0_to_N")
+    x = wl.make_inputs(w, seed=23, cfg_key=2300)
+    units = wl.sample_units(w, 4)
+    S0 = warm_state(w, units, 23, 2301)
+    S0_all = np.zeros((w.units, 128, 128), dtype=np.float32)
+    S0_all[units] = S0
+    say("[gpu] prefill T=%d over %d units" % (T, w.units))
+    dev = lambda a, d=torch.float32: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV).to(d)
+    S_T, o = tw.treewy_chain_prefill(dev(S0_all.reshape(B, H, 128, 128)), dev(x["q"], torch.bfloat16),
+                                     dev(x["k"], torch.bfloat16), dev(x["v"], torch.bfloat16), dev(x["alpha"]),
+                                     dev(x["beta"]))
+    torch.cuda.synchronize()
+    uv = lambda a: a.reshape(w.units, *a.shape[2:])[units]
+    S_ref = oracle.chain(S0, uv(x["k"]), uv(x["v"]), uv(x["alpha"]), uv(x["beta"]))
+    par = np.tile(np.arange(-1, T - 1, dtype=np.int32), (len(units), 1))
+    o_ref, _ = oracle.verify(S0, uv(x["q"]), uv(x["k"]), uv(x["v"]), uv(x["alpha"]), uv(x["beta"]), par)
+    es = assert_close("S_T", S_T.float().cpu().numpy().reshape(w.units, 128, 128)[units], S_ref, TOL["bf16"])
+    eo = assert_close("o", o.float().cpu().numpy().reshape(w.units, T, 128)[units], o_ref, TOL["bf16"])
+    say("[gpu] prefill T=%d: max rel err S_T %.2e o %.2e" % (T, es, eo))
