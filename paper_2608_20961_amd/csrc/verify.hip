@@ -400,9 +400,13 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 
         // Fused commit, per thread: one k chunk (KCH elements of d_k) and one
         // U chunk (4 of d_v) of the CL path rows staged per pass.
-        constexpr int KCH = F32IN ? 4 : 8, KCPR = D / KCH;
-        const int kl = tid / KCPR, kc = (tid % KCPR) * KCH;
-        const int ul = tid / 32, uc = (tid % 32) * 4;
+        // Fused commit, per thread: column sc of the path rows (d_k of k, d_v
+        // of U) at path entries 4 sh .. 4 sh + 3 of the CL staged per pass,
+        // loaded one entry at a time (a wave's 64 columns of one row per
+        // instruction) and stored as one contiguous piece of the transposed
+        // row, so that a wave's store covers distinct banks.
+        static_assert(THREADS == 2 * D && CL == 8, "two 4-entry halves of every column");
+        const int sc = tid % D, sh = tid / D;
         constexpr int OOB = 1 << 30;                     // past every descriptor: reads zero
         const rsrc_t rkp = make_rsrc(FUSE ? static_cast<const In *>(cm.k) + (size_t)u * cm.in_stride * D : nullptr,
                                      FUSE ? cm.N_prev * D * (int)sizeof(In) : 0);
@@ -410,22 +414,33 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                                      FUSE ? cm.N_prev * D * 4 : 0);
         const int *c_node = meta_node(buf);
         const float *c_w = meta_w(buf);
-        // Rows past the path read as zero (out-of-range offset) with weight 0.
-        auto stage_load = [&](int l0, int clen, uint4 &kv, f32x4 &uv) {
-            const int ak = (kl < CL && l0 + kl < clen) ? c_node[l0 + kl] : -1;
-            const int au = l0 + ul < clen ? c_node[l0 + ul] : -1;
-            kv = ld_u32x4<CACHED>(rkp, ak >= 0 ? (ak * D + kc) * (int)sizeof(In) : OOB);
-            uv = ld_f32x4<CACHED>(rup, au >= 0 ? (au * D + uc) * 4 : OOB);
+        // Entries past the path read as zero (out-of-range offset) with weight 0.
+        struct PathPiece {
+            In k[4];
+            float u[4];
         };
-        auto stage_store = [&](int l0, const uint4 &kv, const f32x4 &uv) {
-            if (kl < CL) {
-                const In *kx = reinterpret_cast<const In *>(&kv);
+        auto stage_load = [&](int l0, int clen, PathPiece &pp) {
 #pragma unroll
-                for (int e = 0; e < KCH; ++e) KpT[(kc + e) * CL + kl] = kx[e];
+            for (int i = 0; i < 4; ++i) {
+                const int l = l0 + 4 * sh + i;
+                const int a = l < clen ? c_node[l] : -1;
+                pp.k[i] = ld_elem<In>(rkp, a >= 0 ? (a * D + sc) * (int)sizeof(In) : OOB);
+                pp.u[i] = ld_f32(rup, a >= 0 ? (a * D + sc) * 4 : OOB);
             }
-            const float uw = c_w[l0 + ul];               // 0 past the path
+        };
+        auto stage_store = [&](int l0, const PathPiece &pp) {
+            In kx[4];
+            float ux[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) UwT[(uc + e) * CL + ul] = uw * uv[e];
+            for (int i = 0; i < 4; ++i) {
+                kx[i] = pp.k[i];
+                ux[i] = c_w[l0 + 4 * sh + i] * pp.u[i];  // 0 past the path
+            }
+            if constexpr (F32IN)
+                *reinterpret_cast<f32x4 *>(KpT + sc * CL + 4 * sh) = *reinterpret_cast<const f32x4 *>(kx);
+            else
+                *reinterpret_cast<bf16x4 *>(KpT + sc * CL + 4 * sh) = *reinterpret_cast<const bf16x4 *>(kx);
+            *reinterpret_cast<f32x4 *>(UwT + sc * CL + 4 * sh) = *reinterpret_cast<const f32x4 *>(ux);
         };
 
         // Reads, in the order they are needed.  Fused: wave 3 first fetches
@@ -434,15 +449,14 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // nodes were found one unit ahead), then the unit's own reads.
         int clen = 0;
         float ga = 1.f;
-        uint4 cp_kv;
-        f32x4 cp_uv;
+        PathPiece cp;
         const int u_next = u + (int)gridDim.x;
         const bool has_next = (long long)u + gridDim.x < units;
         if constexpr (FUSE) {
             clen = *meta_len(buf);
             ga = *meta_ga(buf);
             if (wave == 3 && has_next) rd.issue_path(cm, u_next, u_next / H, lane);
-            stage_load(0, clen, cp_kv, cp_uv);
+            stage_load(0, clen, cp);
         }
         // (one workgroup per CU only: at two, the other workgroup hides the loads)
         constexpr bool AHEAD = PRE && F32IN;             // the chain prefill fetches the next chunk early
@@ -513,7 +527,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // Fused: the path rows (first in line) go to LDS, and wave 3, idle
         // here, turns the next unit's path into metadata.
         if constexpr (FUSE) {
-            stage_store(0, cp_kv, cp_uv);
+            stage_store(0, cp);
             if (wave == 3 && has_next) path_meta(u_next, buf ^ 1, lane);
         }
         // K and Q into LDS as bf16 (hi/lo for fp32 input), padding rows zero,
@@ -678,10 +692,9 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             for (int l0 = 0; l0 < clen; l0 += CL) {      // uniform loop
                 if (l0 > 0) {
                     __syncthreads();
-                    uint4 kv;
-                    f32x4 uv;
-                    stage_load(l0, clen, kv, uv);
-                    stage_store(l0, kv, uv);
+                    PathPiece pp;
+                    stage_load(l0, clen, pp);
+                    stage_store(l0, pp);
                     __syncthreads();
                 }
 #pragma unroll
