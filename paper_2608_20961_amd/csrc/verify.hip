@@ -48,7 +48,8 @@
 // writes it out as S_new; MODE walks a unit's nodes in 64-node chunks,
 // either as a chain whose state is carried in registers from chunk to chunk
 // and updated at the end of each (the chain prefill), or as a tree of more
-// than 64 nodes, each chunk reading S0 again and coupled to the pseudo-values
+// than 64 nodes, each chunk using S0 (read again per chunk for an fp32
+// state, kept in registers for a bf16 one) and coupled to the pseudo-values
 // of its ancestors in earlier chunks before its own solve.
 #include "device.h"
 #include "launch.h"
@@ -279,7 +280,7 @@ __device__ __forceinline__ void sweep_column(float (&r)[32], const float *Bm, in
 // How a unit's nodes are walked: in one pass (at most 64 nodes), as a chain
 // in chunks of 64 tokens with the state carried between chunks (chain
 // prefill), or as a tree of more than 64 nodes in chunks of 64, each chunk
-// reading S0 again and coupled to the earlier chunks.
+// using S0 again and coupled to the earlier chunks.
 constexpr int ONE_PASS = 0, CHAIN_PREFILL = 1, TREE_CHUNKS = 2;
 
 // Two workgroups per CU where 256 registers per lane suffice; fp32 inputs
@@ -460,9 +461,13 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         }
         // (one workgroup per CU only: at two, the other workgroup hides the loads)
         constexpr bool AHEAD = PRE && F32IN;             // the chain prefill fetches the next chunk early
+        // Tree chunks read S0 again for every chunk, except with a bf16 state:
+        // its 32 registers stay live from the first chunk without spills (the
+        // fp32 state's 64 do not fit beside the coupling).
+        constexpr bool RELOAD_STATE = XT && !SBF;
         if (!AHEAD || chunk == 0)                        // (then later chunks were fetched one chunk ahead)
-            rd.template issue<XT ? CACHED : STREAM>(S0, q, k, v, alpha, beta, prow, u, N, node0, chunk == 0 || XT,
-                                                    tid, lane, wave, hg, col);
+            rd.template issue<XT ? CACHED : STREAM>(S0, q, k, v, alpha, beta, prow, u, N, node0,
+                                                    chunk == 0 || RELOAD_STATE, tid, lane, wave, hg, col);
 
         // ---- phase 1: ancestors and cumulative decay by pointer jumping ----
         // Lane t of wave 0 keeps (ptr, prod, mask): ptr an ancestor of t (or
