@@ -140,7 +140,7 @@ def dataclass_replace(w, **kw):
 
 
 # ---------------------------------------------------------------------------
-# Commit semantics, determinism, rounds
+# Commit semantics, determinism, consecutive speculation steps
 # ---------------------------------------------------------------------------
 def test_empty_path_and_in_place_commit(tw):
     w = wl.scaled(wl.WORKLOADS[1], B=6, H=4)
@@ -188,7 +188,7 @@ def test_deterministic(tw):
         assert torch.equal(a, b)
 
 
-def test_two_rounds_equal_one_longer_chain(tw):
+def test_two_steps_equal_one_longer_chain(tw):
     """Verify+commit a chain of 8, then verify the next 8 from the committed
     state: matches the oracle's chain of 16 (committed state = next S0)."""
     w16 = wl.Workload("chain16", 2, 3, 16, 128, 128, "bf16", "chain", 16, (1,), (0.85, 0.999),
@@ -207,7 +207,7 @@ def test_two_rounds_equal_one_longer_chain(tw):
     o2, _ = tw.treewy_verify(S1, sub["q"], sub["k"], sub["v"], sub["alpha"], sub["beta"], par8)
     torch.cuda.synchronize()
     got = units_of(o2, wl.scaled(w16, N=8), case.check)
-    assert_close("round 2 o", got, o_ref[:, 8:16], TOL["bf16"])
+    assert_close("second step o", got, o_ref[:, 8:16], TOL["bf16"])
 
 
 # ---------------------------------------------------------------------------
