@@ -94,6 +94,15 @@ def test_full_size_sampled(tw):
     check(tw, Case(w, seed=0, cfg_key=1500, check_units=wl.sample_units(w, 16)), "397B-tree128 full")
 
 
+def test_full_size_sampled_bf16_state(tw):
+    """The same launch with a bf16 state, which stays in registers from the
+    first 64-node chunk to the second instead of being read again."""
+    w = wl.BIG_TREE
+    case = Case(w, seed=1, cfg_key=1510, check_units=wl.sample_units(w, 16))
+    case.S0 = wl.round_to_bf16(case.S0)              # the state as stored: bf16 values
+    check(tw, case, "397B-tree128 full", state="bf16")
+
+
 def test_long_path_commit_full_chain(tw):
     """Commit of every node of a 256-chain (L_max = 256, four staging passes)."""
     N = 256
