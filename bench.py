@@ -3,17 +3,23 @@
 A step is one pass of the hot path over one batch: treewy_verify (every draft
 node's output and the pseudo-values, one solve per (sequence, head)) followed
 by treewy_commit (the accepted node's state, out of place so the inputs stay
-fixed).  The default workload is the 397B-shaped wide tree: B = 128 sequences,
-H = 64 value heads, d_k = d_v = 128, N = 64 draft nodes (max depth 8), bf16
-q/k/v and fp32 state.  Inputs are resident in HBM before the timed region.
+fixed).  The headline workload is the 397B-shaped wide tree: B = 128
+sequences, H = 64 value heads, d_k = d_v = 128, N = 64 draft nodes (max depth
+8), bf16 q/k/v and fp32 state.  Inputs are resident in HBM before the timed
+region.
 
 Prints ONE JSON line.  Besides the headline (verified draft nodes per second
-for the layer) it carries the per-kernel HBM rooflines, the full-state-
-snapshot baseline on the same workload, and the float64 oracle timed on the
-host's cores as a CPU baseline.
+for the layer) it carries the per-kernel HBM rooflines, a block per other
+workload (the 4-node fp32 chain, the 35B-shaped chain and tree, and the
+32-node stress tree with the full-state-snapshot comparison: bytes moved and
+speculative memory of both methods), the fused call, the bf16 state, the chain
+prefill, 128-node trees, and the float64 oracle timed on the host's cores as
+a CPU baseline.  The other workloads run first and the headline after them,
+so that its steps run at the clocks the GPU holds under sustained load.
 
   python bench.py [--steps K] [--warmup W] [--workload 0..4] [--gpus 1]
-                  [--no-snapshot] [--no-cpu-baseline] [--copy-calibration]
+                  [--configs 0,1,2,4 | --no-configs] [--no-snapshot]
+                  [--no-cpu-baseline] [--copy-calibration]
 """
 from __future__ import annotations
 
@@ -53,6 +59,11 @@ def parse():
                    help="tokens per sequence for the chain-prefill measurement (0 skips it)")
     p.add_argument("--no-big-tree", action="store_true", help="skip the 128-node tree (chunked verify)")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time for the CPU baseline")
+    p.add_argument("--configs", default="0,1,2,4",
+                   help="other workloads measured first, each in a block of its own (comma-separated ids)")
+    p.add_argument("--no-configs", action="store_true", help="skip the other workloads' blocks")
+    p.add_argument("--config-cpu-seconds", type=float, default=2.0,
+                   help="target oracle time for each other workload's CPU baseline")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain 1 GiB device copy (for scaling HBM counters)")
     return p.parse_args()
@@ -196,11 +207,13 @@ def _cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(w, wl, x, seed, target_s):
+def cpu_baseline(w, wl, x, seed, target_s, max_units=None):
     """The float64 oracle (verify + commit) on a bounded sample of units.
 
     S0 of each sampled unit is the oracle's own warm-up over the unit's
-    warm-up tokens (untimed); the timed part is verify + commit."""
+    warm-up tokens (untimed); the timed part is verify + commit.  The sample
+    grows from a 64-unit probe to about `target_s` seconds of oracle time, and
+    at most `max_units` units."""
     import oracle
     orc = oracle.default()
     H, N = w.H, w.N
@@ -228,6 +241,8 @@ def cpu_baseline(w, wl, x, seed, target_s):
     probe = np.arange(min(64, w.units))
     dt = run(probe, warm(probe))
     count = int(min(w.units, max(len(probe), len(probe) * target_s / max(dt, 1e-6))))
+    if max_units is not None:
+        count = max(len(probe), min(count, max_units))
     units = wl.sample_units(w, count, seed=1)
     dt = run(units, warm(units))
     nodes_per_s = (len(units) / H) * N / dt       # a sequence's N nodes cost H units of work
@@ -235,6 +250,119 @@ def cpu_baseline(w, wl, x, seed, target_s):
             "cpu_model": _cpu_model(), "host_cpus": os.cpu_count(),
             "sample": "%d of %d (sequence, head) units of the same workload; float64 verify + commit "
                       "took %.2f s; nodes/s = units/H * N / time" % (len(units), w.units, dt)}
+
+
+def make_flush(torch, acc, w, path_len):
+    """A workload whose step fits in the 256 MiB last-level cache would be
+    served from it step after step: then 512 MiB are read between steps
+    (outside the timed launches).  A read leaves the caches holding clean
+    lines; a write (zero-fill) would leave dirty ones, whose write-back the
+    next timed launch would pay for (at the 16-node workload that cost verify
+    60%).  None for workloads that do not fit."""
+    if acc.verify_bytes(w) + acc.commit_bytes(w, path_len) >= (1 << 30):
+        return None
+    scratch = torch.ones(1 << 27, device="cuda")
+
+    def flush():
+        scratch.max()
+    return flush
+
+
+def snapshot_comparison(torch, tw, acc, w, x, d, o, ms_treewy_step, steps):
+    """Full-state snapshotting (approach (i) of Section "The memory problem")
+    on the same inputs: its verify writes every node's state, its commit
+    copies the accepted one.  Reports time, bytes moved and speculative
+    memory for both methods.  The snapshot buffer is allocated here and freed
+    before returning."""
+    S_new = torch.empty_like(d["S0"])
+    snaps = torch.empty((w.B, w.H, w.N, w.d_v, w.d_k), dtype=torch.float32, device="cuda")
+    acc_node = torch.tensor([int(x["path"][b, x["path_len"][b] - 1]) if x["path_len"][b] else -1
+                             for b in range(w.B)], dtype=torch.int32, device="cuda")
+    o2 = torch.empty_like(o)
+
+    def sverify():
+        tw.treewy_snapshot_verify(d["S0"], d["q"], d["k"], d["v"], d["alpha"], d["beta"], d["parent"],
+                                  o=o2, snapshots=snaps)
+
+    def scommit():
+        tw.treewy_snapshot_commit(d["S0"], snaps, acc_node, S_new=S_new)
+
+    ms_s, (ms_sv, ms_sc) = time_steps(torch, [sverify, scommit], steps, 1)
+    sb = acc.snapshot_verify_bytes(w)
+    reload = acc.snapshot_reload_bytes(w, x["parent"])
+    spec = acc.speculative_state_bytes(w)
+    tw_bytes = acc.verify_bytes(w) + acc.commit_bytes(w, x["path_len"])
+    snap_bytes = sb + acc.snapshot_commit_bytes(w)
+    out = {
+        "workload": w.describe(), "ms_per_step": round(ms_s, 4), "steps": steps,
+        "nodes_per_s": round(w.B * w.N / (ms_s * 1e-3), 1),
+        "verify": dict(roofline(sb, ms_sv, None), parent_reload_bytes=int(reload),
+                       frac_with_reloads=round((sb + reload) / (ms_sv * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)),
+        "commit": roofline(acc.snapshot_commit_bytes(w), ms_sc, None),
+        "bytes_moved_per_step": {"treewy": int(tw_bytes), "snapshot": int(snap_bytes),
+                                 "snapshot_with_reloads": int(snap_bytes + reload),
+                                 "ratio": round(snap_bytes / tw_bytes, 2)},
+        "speculative_state_bytes": {"treewy_U": spec["treewy_U"], "treewy_U_k_alpha": spec["treewy_U_k_alpha"],
+                                    "snapshot_states": spec["snapshot_states"],
+                                    "committed_state": spec["committed_state"],
+                                    "ratio_U": round(spec["snapshot_states"] / spec["treewy_U"], 1)},
+        "treewy_speedup": round(ms_s / ms_treewy_step, 2),
+    }
+    del snaps, S_new, o2
+    return out
+
+
+def measure_workload(torch, tw, wl, acc, w, args, src_hash, cpu_seconds, snapshot):
+    """One workload's block: verify + commit steps (the headline's step on
+    this workload), the fused call, optionally the snapshot comparison, and
+    the oracle's CPU baseline on a bounded sample."""
+    x, d = device_inputs(torch, tw, wl, w, args.seed)
+    U = torch.empty((w.B, w.H, w.N, w.d_v), dtype=torch.float32, device="cuda")
+    o = torch.empty((w.B, w.H, w.N, w.d_v), dtype=d["q"].dtype, device="cuda")
+    S_new = torch.empty_like(d["S0"])
+    S0_commit = d["S0"].clone()
+
+    def verify():
+        tw.treewy_verify(d["S0"], d["q"], d["k"], d["v"], d["alpha"], d["beta"], d["parent"], o=o, U=U)
+
+    def commit():
+        tw.treewy_commit(S0_commit, U, d["k"], d["alpha"], d["path"], d["path_len"], parent=d["parent"],
+                         S_new=S_new)
+
+    flush = make_flush(torch, acc, w, x["path_len"])
+    dist = []
+    ms_step, (ms_v, ms_c) = time_steps(torch, [verify, commit], args.steps, args.warmup, flush, dist)
+    S_f, o_f, U_f = torch.empty_like(d["S0"]), torch.empty_like(o), torch.empty_like(U)
+
+    def fused():
+        tw.treewy_commit_verify(S0_commit, U, d["k"], d["alpha"], d["path"], d["path_len"], d["q"], d["k"], d["v"],
+                                d["alpha"], d["beta"], d["parent"], parent_prev=d["parent"], S_new=S_f, o=o_f,
+                                U=U_f)
+
+    _, (ms_f,) = time_steps(torch, [fused], args.steps, args.warmup, flush)
+    nodes = w.B * w.N
+    block = {
+        "workload": w.describe(), "units": w.units, "ms_per_step": round(ms_step, 5),
+        "nodes_per_s": round(nodes / (ms_step * 1e-3), 1), "cache_flushed_between_steps": flush is not None,
+        "verify": dict(roofline(acc.verify_bytes(w), ms_v, load_traffic("verify", w.name, src_hash)),
+                       launch_ms_p10_p50_p90=dist[0], nodes_per_s=round(nodes / (ms_v * 1e-3), 1)),
+        "commit": dict(roofline(acc.commit_bytes(w, x["path_len"]), ms_c, load_traffic("commit", w.name, src_hash)),
+                       launch_ms_p10_p50_p90=dist[1]),
+        "fused_commit_verify": dict(roofline(acc.commit_verify_bytes(w, x["path_len"]), ms_f,
+                                             load_traffic("commit_verify", w.name, src_hash)),
+                                    speedup_vs_separate_calls=round(ms_step / ms_f, 3)),
+    }
+    log("%s: verify %.4f, commit %.4f, fused %.4f ms" % (w.name, ms_v, ms_c, ms_f))
+    del S_f, o_f, U_f
+    if snapshot:
+        block["snapshot_comparison"] = snapshot_comparison(torch, tw, acc, w, x, d, o, ms_step,
+                                                           max(3, args.steps // 10))
+        log("%s: snapshot baseline %.4f ms/step" % (w.name, block["snapshot_comparison"]["ms_per_step"]))
+    if cpu_seconds > 0:
+        block["cpu_baseline"] = cpu_baseline(w, wl, x, args.seed, cpu_seconds, max_units=2048)
+    del d, U, o, S_new, S0_commit
+    torch.cuda.empty_cache()
+    return block
 
 
 def main():
@@ -251,8 +379,22 @@ def main():
     from paper_2608_20961_amd import treewy as tw
     from paper_2608_20961_amd import workload as wl
 
+    src_hash = kernel_source_hash()
+    # The other workloads first, each in a block of its own (the 32-node
+    # stress tree with the snapshot comparison it exists for).
+    others = {}
+    if not args.no_configs:
+        for i in [int(c) for c in args.configs.split(",") if c.strip() != ""]:
+            if i == args.workload:
+                continue
+            wo = wl.WORKLOADS[i]
+            log("workload " + wo.describe())
+            others[wo.name] = measure_workload(torch, tw, wl, acc, wo, args, src_hash,
+                                               0 if args.no_cpu_baseline else args.config_cpu_seconds,
+                                               snapshot=not args.no_snapshot and wo.name == "stress-tree32")
+
     w = wl.WORKLOADS[args.workload]
-    log("workload " + w.describe())
+    log("workload " + w.describe() + " (headline)")
     x, d = device_inputs(torch, tw, wl, w, args.seed)
     log("inputs resident, S0 warmed on the device")
     U = torch.empty((w.B, w.H, w.N, w.d_v), dtype=torch.float32, device="cuda")
@@ -272,22 +414,10 @@ def main():
         tw.treewy_commit(S0_commit, U, d["k"], d["alpha"], d["path"], d["path_len"], parent=d["parent"],
                          S_new=S_new)
 
-    # A workload whose step fits in the 256 MiB last-level cache would be
-    # served from it step after step: then 512 MiB are read between steps
-    # (outside the timed launches).  A read leaves the caches holding clean
-    # lines; a write (zero-fill) would leave dirty ones, whose write-back the
-    # next timed launch would pay for (at the 16-node workload that cost
-    # verify 60%).
-    flush = None
-    if acc.verify_bytes(w) + acc.commit_bytes(w, x["path_len"]) < (1 << 30):
-        scratch = torch.ones(1 << 27, device="cuda")
-
-        def flush():
-            scratch.max()
+    flush = make_flush(torch, acc, w, x["path_len"])
     dist = []
     ms_step, (ms_verify, ms_commit) = time_steps(torch, [verify, commit], args.steps, args.warmup, flush, dist)
     log("timed %d steps: %.4f ms/step (verify %.4f, commit %.4f)" % (args.steps, ms_step, ms_verify, ms_commit))
-    src_hash = kernel_source_hash()
     vb = acc.verify_bytes(w)
     cb = acc.commit_bytes(w, x["path_len"])
     rf_verify = roofline(vb, ms_verify, load_traffic("verify", w.name, src_hash))
@@ -305,7 +435,8 @@ def main():
         "config": {"workload": w.describe(), "B": w.B, "H": w.H, "N": w.N, "d_k": w.d_k, "d_v": w.d_v,
                    "step": "treewy_verify + treewy_commit (out of place)", "accumulate": "f32",
                    "state": "f32", "parallelism": "none (1 GPU)",
-                   "cache_flushed_between_steps": flush is not None},
+                   "cache_flushed_between_steps": flush is not None,
+                   "measured_after": sorted(others)},
         "roofline": dict(dominant, kernel="treewy_verify" if dominant is rf_verify else "treewy_commit"),
         "verify": dict(rf_verify, launch_ms_p10_p50_p90=dist[0], nodes_per_s=round(nodes / (ms_verify * 1e-3), 1),
                        head_nodes_per_s=round(w.units * w.N / (ms_verify * 1e-3), 1),
@@ -325,7 +456,7 @@ def main():
                                 d["alpha"], d["beta"], d["parent"], parent_prev=d["parent"], S_new=S_fused, o=o_f,
                                 U=U_f)
 
-    _, (ms_fused,) = time_steps(torch, [fused], args.steps, args.warmup)
+    _, (ms_fused,) = time_steps(torch, [fused], args.steps, args.warmup, flush)
     log("fused commit+verify: %.4f ms/launch" % ms_fused)
     fb = acc.commit_verify_bytes(w, x["path_len"])
     result["fused_commit_verify"] = dict(
@@ -354,8 +485,8 @@ def main():
                                     S_new=S_new_b, o=o_f2, U=U_f2)
 
         o_f2, U_f2 = torch.empty_like(o), torch.empty_like(U)
-        ms_step_b, (ms_vb, ms_cb) = time_steps(torch, [verify_b, commit_b], args.steps, args.warmup)
-        _, (ms_fb,) = time_steps(torch, [fused_b], args.steps, args.warmup)
+        ms_step_b, (ms_vb, ms_cb) = time_steps(torch, [verify_b, commit_b], args.steps, args.warmup, flush)
+        _, (ms_fb,) = time_steps(torch, [fused_b], args.steps, args.warmup, flush)
         log("bf16 state: verify %.4f, commit %.4f, fused %.4f ms" % (ms_vb, ms_cb, ms_fb))
         result["bf16_state"] = {
             "ms_per_step": round(ms_step_b, 5), "nodes_per_s": round(nodes / (ms_step_b * 1e-3), 1),
@@ -444,30 +575,11 @@ def main():
     result["speculative_state_bytes"] = {"treewy_U": spec["treewy_U"], "treewy_U_k_alpha": spec["treewy_U_k_alpha"],
                                          "snapshot_states": spec["snapshot_states"]}
     if not args.no_snapshot:
-        snaps = torch.empty((w.B, w.H, w.N, w.d_v, w.d_k), dtype=torch.float32, device="cuda")
-        acc_node = torch.tensor([int(x["path"][b, x["path_len"][b] - 1]) if x["path_len"][b] else -1
-                                 for b in range(w.B)], dtype=torch.int32, device="cuda")
-        o2 = torch.empty_like(o)
-
-        def sverify():
-            tw.treewy_snapshot_verify(d["S0"], d["q"], d["k"], d["v"], d["alpha"], d["beta"], d["parent"],
-                                      o=o2, snapshots=snaps)
-
-        def scommit():
-            tw.treewy_snapshot_commit(d["S0"], snaps, acc_node, S_new=S_new)
-
-        ss = max(3, args.steps // 10)
-        ms_s, (ms_sv, ms_sc) = time_steps(torch, [sverify, scommit], ss, 1)
-        sb = acc.snapshot_verify_bytes(w)
-        result["snapshot_baseline"] = {
-            "ms_per_step": round(ms_s, 4), "steps": ss,
-            "nodes_per_s": round(nodes / (ms_s * 1e-3), 1),
-            "verify": roofline(sb, ms_sv, None), "commit": roofline(acc.snapshot_commit_bytes(w), ms_sc, None),
-            "speculative_state_bytes": spec["snapshot_states"],
-            "treewy_speedup": round(ms_s / ms_step, 2),
-        }
-        del snaps
-        log("snapshot baseline: %.4f ms/step" % ms_s)
+        result["snapshot_baseline"] = snapshot_comparison(torch, tw, acc, w, x, d, o, ms_step,
+                                                          max(3, args.steps // 10))
+        log("snapshot baseline: %.4f ms/step" % result["snapshot_baseline"]["ms_per_step"])
+    if others:
+        result["configs"] = others
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
         result["cpu_baseline"] = cpu_baseline(w, wl, x, args.seed, args.cpu_seconds)

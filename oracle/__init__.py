@@ -55,18 +55,23 @@ def _ptr(a: Optional[np.ndarray]):
 
 
 class Oracle:
-    """Bound to one compiled oracle library."""
+    """Bound to one compiled oracle library.
 
-    def __init__(self, lib_path: str = LIB_PATH):
-        lib = ctypes.CDLL(lib_path)
-        P, I = ctypes.c_void_p, ctypes.c_int
-        lib.oracle_threads.restype = I
-        lib.oracle_gdn_tree.argtypes = [I, I, I, I] + [P] * 10
-        lib.oracle_gdn_tree.restype = I
-        lib.oracle_gdn_chain.argtypes = [I, I, I, I] + [P] * 5
-        lib.oracle_gdn_chain.restype = I
-        lib.oracle_commit.argtypes = [I, I, I, I, I] + [P] * 9
-        lib.oracle_commit.restype = I
+    `lib` may instead be any object with the library's four functions and the
+    same arguments (sizes as ints, arrays as ctypes pointers): the test suite
+    passes one that forwards each call to a sanitizer build of oracle.c."""
+
+    def __init__(self, lib_path: str = LIB_PATH, lib=None):
+        if lib is None:
+            lib = ctypes.CDLL(lib_path)
+            P, I = ctypes.c_void_p, ctypes.c_int
+            lib.oracle_threads.restype = I
+            lib.oracle_gdn_tree.argtypes = [I, I, I, I] + [P] * 10
+            lib.oracle_gdn_tree.restype = I
+            lib.oracle_gdn_chain.argtypes = [I, I, I, I] + [P] * 5
+            lib.oracle_gdn_chain.restype = I
+            lib.oracle_commit.argtypes = [I, I, I, I, I] + [P] * 9
+            lib.oracle_commit.restype = I
         self._lib = lib
         self.path = lib_path
 

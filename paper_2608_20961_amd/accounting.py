@@ -15,6 +15,8 @@ element size (2 for bf16, 4 for fp32), state and pseudo-values in fp32:
              + N*d*s_in (o) + N*d*4 (U)               + N*4/H (parent, shared by heads)
   commit   = 2*d^2*4 (S0 read, S_new write) + L*(d*4 + d*s_in + 4) (U, k, alpha on the path)
   snapshot = d^2*4 + inputs + o + N*d^2*4 (one full state written per node)
+             (+ d^2*4 per node whose parent is not the node before it, read
+             back by the node-by-node baseline kernel; counted separately)
 """
 from __future__ import annotations
 
@@ -96,9 +98,23 @@ def prefill_bytes(w: Workload, T: int, state_bytes: int = 4) -> int:
 
 
 def snapshot_verify_bytes(w: Workload) -> int:
+    """What store-all must move at least: S0 once, the node vectors, o, and
+    one full state written per node (an ideal kernel keeps the states of the
+    current root-to-node path on chip, so it never reads a snapshot back)."""
     s, d, N = elem_bytes(w.in_dtype), w.d_k, w.N
     per_unit = d * d * 4 + 3 * N * d * s + 2 * N * 4 + N * d * s + N * d * d * 4
     return w.units * per_unit + w.B * N * 4
+
+
+def snapshot_reload_bytes(w: Workload, parent: np.ndarray) -> int:
+    """State bytes the baseline kernel reads back on top of that: the node-by-
+    node kernel holds one running state, so every node whose parent is not the
+    node before it reloads its parent's state (S0 or a snapshot, d^2 fp32
+    values).  parent [B, N]."""
+    par = np.asarray(parent, dtype=np.int64)
+    prev = np.arange(-1, w.N - 1, dtype=np.int64)[None, :]
+    reloads = int((par != prev).sum())               # per sequence, summed over B
+    return reloads * w.H * w.d_k * w.d_v * 4
 
 
 def snapshot_commit_bytes(w: Workload) -> int:

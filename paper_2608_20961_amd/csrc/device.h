@@ -140,6 +140,30 @@ __device__ __forceinline__ uint2 f32_to_bf4(f32x4 x) {
     return __builtin_bit_cast(uint2, h);
 }
 
+// Cumulative decays in extended range.  g_t, a product of up to 256 gates in
+// (0, 1], is held as g = m 2^e with m in [0.5, 1) (m = e = 0 for a padding
+// node): the product of many small gates cannot underflow, and a ratio
+// g_t / g_i (i an ancestor of t, so at most 1) is formed as
+// (m_t / m_i) 2^(e_t - e_i) and cannot overflow.  Scaling by a power of two
+// is exact, so wherever the plain fp32 products stay normal these give the
+// same bits as g_t * (1 / g_i).
+struct DecayX {
+    // a = a * b, renormalised
+    static __device__ __forceinline__ void mul(float &m, int &e, float mb, int eb) {
+        m *= mb;
+        e += eb + __builtin_amdgcn_frexp_expf(m);
+        m = __builtin_amdgcn_frexp_mantf(m);
+    }
+    static __device__ __forceinline__ float mant(float x) { return __builtin_amdgcn_frexp_mantf(x); }
+    static __device__ __forceinline__ int expo(float x) { return __builtin_amdgcn_frexp_expf(x); }
+    // the plain value (tiny values round to a denormal or zero, as they should)
+    static __device__ __forceinline__ float value(float m, int e) { return __builtin_amdgcn_ldexpf(m, e); }
+    // g_t / g_i from g_t = (mt, et) and 1 / m_i, e_i
+    static __device__ __forceinline__ float ratio(float mt, int et, float inv_mi, int ei) {
+        return __builtin_amdgcn_ldexpf(mt * inv_mi, et - ei);
+    }
+};
+
 __device__ __forceinline__ float to_f32(float x) { return x; }
 __device__ __forceinline__ float to_f32(__bf16 x) { return (float)x; }
 

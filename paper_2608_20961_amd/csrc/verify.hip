@@ -51,6 +51,8 @@
 // than 64 nodes, each chunk using S0 (read again per chunk for an fp32
 // state, kept in registers for a bf16 one) and coupled to the pseudo-values
 // of its ancestors in earlier chunks before its own solve.
+#include <atomic>
+
 #include "device.h"
 #include "launch.h"
 
@@ -83,8 +85,9 @@ struct VerifyLds {
     static constexpr int M_BYTES = NP * MS * 4;
     static constexpr int A_OFF = B_OFF + M_BYTES;
     static constexpr int BETA_OFF = A_OFF + M_BYTES;
-    static constexpr int G_OFF = BETA_OFF + NP * 4;
-    static constexpr int ANC_OFF = G_OFF + NP * 4;
+    static constexpr int G_OFF = BETA_OFF + NP * 4;     // cumulative decays: mantissas ...
+    static constexpr int GE_OFF = G_OFF + NP * 4;       // ... and exponents (see DecayX)
+    static constexpr int ANC_OFF = GE_OFF + NP * 4;
     static constexpr int FLAG_OFF = ANC_OFF + NP * 8;   // 1 when every node has <= FAST ancestors
     static constexpr int END = FLAG_OFF + 16;
     static constexpr bool O_IN_B = NP * OS * 2 <= M_BYTES;   // o staged where B was, else appended
@@ -104,13 +107,14 @@ struct VerifyLds {
     static constexpr int UWT_OFF = KPT_OFF + D * CL * (F32IN ? 4 : 2);
     static constexpr int BYTES = FUSE ? UWT_OFF + D * CL * 4 : BASE_BYTES;
     // Trees of more than 64 nodes, walked in chunks of 64: every node's
-    // cumulative decay and ancestor mask (one word per chunk).  With bf16
-    // inputs this still fits two workgroups per CU.
+    // cumulative decay (mantissa, exponent) and ancestor mask (one word per
+    // chunk).  With bf16 inputs this still fits two workgroups per CU.
     static constexpr int GALL_OFF = BASE_BYTES;
-    static constexpr int ANCALL_OFF = GALL_OFF + MAX_TREE * 4;
+    static constexpr int GEALL_OFF = GALL_OFF + MAX_TREE * 4;
+    static constexpr int ANCALL_OFF = GEALL_OFF + MAX_TREE * 4;
     static constexpr int TREE_BYTES = ANCALL_OFF + MAX_TREE * MASK_WORDS * 8;
     static_assert(NP * US * 4 <= B_OFF, "U staging must fit where K/Q were staged");
-    static_assert(B_OFF % 16 == 0 && A_OFF % 16 == 0 && BETA_OFF % 16 == 0 && G_OFF % 16 == 0 &&
+    static_assert(B_OFF % 16 == 0 && A_OFF % 16 == 0 && BETA_OFF % 16 == 0 && G_OFF % 16 == 0 && GE_OFF % 16 == 0 &&
                   ANC_OFF % 32 == 0 && O_OFF % 16 == 0 && V_OFF % 16 == 0 &&
                   KPT_OFF % 16 == 0 && UWT_OFF % 16 == 0 && ANCALL_OFF % 16 == 0, "alignment");
 };
@@ -312,10 +316,12 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
     float *Us = reinterpret_cast<float *>(lds);          // U is staged where K/Q were, after P
     __bf16 *Os = reinterpret_cast<__bf16 *>(lds + L::O_OFF);   // o staging (bf16 input only)
     float *be_s = reinterpret_cast<float *>(lds + L::BETA_OFF);
-    float *g_s = reinterpret_cast<float *>(lds + L::G_OFF);
+    float *gm_s = reinterpret_cast<float *>(lds + L::G_OFF);  // g_t = gm_s[t] 2^ge_s[t] (DecayX)
+    int *ge_s = reinterpret_cast<int *>(lds + L::GE_OFF);
     uint64_t *anc_s = reinterpret_cast<uint64_t *>(lds + L::ANC_OFF);
     int *shallow_s = reinterpret_cast<int *>(lds + L::FLAG_OFF);
-    float *g_all = reinterpret_cast<float *>(lds + L::GALL_OFF);            // (tree chunks)
+    float *gm_all = reinterpret_cast<float *>(lds + L::GALL_OFF);           // (tree chunks)
+    int *ge_all = reinterpret_cast<int *>(lds + L::GEALL_OFF);
     uint64_t *anc_all = reinterpret_cast<uint64_t *>(lds + L::ANCALL_OFF);
     constexpr int FAST = 8;                              // ancestors a lane holds in registers
     // fused commit staging (unused otherwise)
@@ -471,24 +477,26 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 
         // ---- phase 1: ancestors and cumulative decay by pointer jumping ----
         // Lane t of wave 0 keeps (ptr, prod, mask): ptr an ancestor of t (or
-        // -1), prod the product of alpha over the path (ptr, t], mask the
-        // ancestors of t strictly below t down to and including ptr.  Each
-        // round doubles the covered path by reading the state of lane ptr, so
-        // depth d needs ceil(log2 d) rounds; then prod = g_t, mask = ancestors.
+        // -1), prod the product of alpha over the path (ptr, t] (in extended
+        // range, DecayX: mantissa pm, exponent pe), mask the ancestors of t
+        // strictly below t down to and including ptr.  Each round doubles the
+        // covered path by reading the state of lane ptr, so depth d needs
+        // ceil(log2 d) rounds; then prod = g_t, mask = ancestors.
         // Tree chunks: a parent in an earlier chunk already has its final
-        // decay and ancestors (g_all, anc_all), so the lane takes them over
-        // at once; ext holds the ancestor words of the earlier chunks.
+        // decay and ancestors (gm_all / ge_all, anc_all), so the lane takes
+        // them over at once; ext holds the ancestor words of the earlier chunks.
         if (wave == 0) {
             int ptr = lane < N ? ((!PRE && parent) ? rd.par : lane - 1) : -1;   // (no parent array: a chain)
             if (lane < N && (ptr < -1 || ptr >= base + lane)) {
                 flag_error(err, b, TREEWY_FLAG_BAD_PARENT);
                 ptr = -1;
             }
-            float prod = lane < N ? rd.al : 0.f;
+            float pm = lane < N ? DecayX::mant(rd.al) : 0.f;
+            int pe = lane < N ? DecayX::expo(rd.al) : 0;
             uint64_t ext[XT ? MASK_WORDS : 1] = {};
             if constexpr (XT) {
                 if (ptr >= 0 && ptr < base) {
-                    prod *= g_all[ptr];
+                    DecayX::mul(pm, pe, gm_all[ptr], ge_all[ptr]);
 #pragma unroll
                     for (int j = 0; j < MASK_WORDS; ++j)
                         ext[j] = anc_all[ptr * MASK_WORDS + j] | (j == (ptr >> 6) ? 1ull << (ptr & 63) : 0ull);
@@ -500,7 +508,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             uint64_t mask = ptr >= 0 ? (1ull << ptr) : 0ull;
             while (__any(ptr >= 0)) {
                 const int src = ptr >= 0 ? ptr : lane;
-                const float prod_s = __shfl(prod, src);
+                const float pm_s = __shfl(pm, src);
+                const int pe_s = __shfl(pe, src);
                 const int ptr_s = __shfl(ptr, src);
                 const uint64_t mask_s = __shfl(mask, src);
                 uint64_t ext_s[XT ? MASK_WORDS : 1] = {};
@@ -508,7 +517,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 #pragma unroll
                     for (int j = 0; j < MASK_WORDS; ++j) ext_s[j] = __shfl(ext[j], src);
                 if (ptr >= 0) {
-                    prod *= prod_s;
+                    DecayX::mul(pm, pe, pm_s, pe_s);
                     mask |= mask_s;
                     ptr = ptr_s;
                     if constexpr (XT)
@@ -517,12 +526,14 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 }
             }
             if (lane < NP) {
-                g_s[lane] = prod;
+                gm_s[lane] = pm;
+                ge_s[lane] = pe;
                 be_s[lane] = lane < N ? rd.be : 0.f;
                 anc_s[lane] = mask;
             }
             if constexpr (XT) {                          // base + lane < MAX_TREE: at most 4 chunks
-                g_all[base + lane] = prod;
+                gm_all[base + lane] = pm;
+                ge_all[base + lane] = pe;
 #pragma unroll
                 for (int j = 0; j < MASK_WORDS; ++j) anc_all[(base + lane) * MASK_WORDS + j] = j == chunk ? mask : ext[j];
             }
@@ -625,14 +636,16 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 }
             }
             const int ci = 32 * nt + l32;
-            const float inv_gi = 1.f / g_s[ci];
+            const float inv_mi = 1.f / gm_s[ci];
+            const int ei = ge_s[ci];
             // The accumulator rows come in runs of four consecutive nodes, so
             // their decays, betas and ancestor masks arrive as 16-byte LDS
             // broadcasts; bit ci of a mask sits in word nt of the row's u64.
 #pragma unroll
             for (int r4 = 0; r4 < 16; r4 += 4) {
                 const int t0 = 32 * mt + acc_row(r4, hg);      // rows t0 .. t0 + 3
-                const f32x4 g4 = *reinterpret_cast<const f32x4 *>(g_s + t0);
+                const f32x4 g4 = *reinterpret_cast<const f32x4 *>(gm_s + t0);
+                const int4 e4 = *reinterpret_cast<const int4 *>(ge_s + t0);
                 const f32x4 b4 = *reinterpret_cast<const f32x4 *>(be_s + t0);
                 const uint4 m01 = *reinterpret_cast<const uint4 *>(anc_s + t0);
                 const uint4 m23 = *reinterpret_cast<const uint4 *>(anc_s + t0 + 2);
@@ -642,7 +655,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 for (int e = 0; e < 4; ++e) {
                     const int r = r4 + e, t = t0 + e;
                     const bool strict = (w[e] >> l32) & 1u;
-                    const float ratio = strict ? g4[e] * inv_gi : (ci == t ? 1.f : 0.f);
+                    const int et = e == 0 ? e4.x : e == 1 ? e4.y : e == 2 ? e4.z : e4.w;
+                    const float ratio = strict ? DecayX::ratio(g4[e], et, inv_mi, ei) : (ci == t ? 1.f : 0.f);
                     Bm[t * MS + ci] = strict ? b4[e] * ratio * gkk[r] : 0.f;
                     Am[t * MS + ci] = ratio * gqk[r];
                 }
@@ -891,19 +905,49 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         __builtin_amdgcn_s_setprio(0);                  // (wave 3 after a deep solve)
         __syncthreads();
 
+        // Decays g_t of four consecutive rows t0 .. t0 + 3, as plain values.
+        auto g_rows4 = [&](int t0) {
+            const f32x4 m4 = *reinterpret_cast<const f32x4 *>(gm_s + t0);
+            const int4 e4 = *reinterpret_cast<const int4 *>(ge_s + t0);
+            return f32x4{DecayX::value(m4[0], e4.x), DecayX::value(m4[1], e4.y), DecayX::value(m4[2], e4.z),
+                         DecayX::value(m4[3], e4.w)};
+        };
+
+        // ---- phase 4: R and g P_Q ---------------------------------------------
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+#pragma unroll
+            for (int r4 = 0; r4 < 16; r4 += 4) {
+                const int t0 = 32 * m + acc_row(r4, hg);
+                const f32x4 g4 = g_rows4(t0);
+                const f32x4 b4 = *reinterpret_cast<const f32x4 *>(be_s + t0);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int r = r4 + e;
+                    float vt;
+                    if constexpr (F32IN)
+                        vt = vr[m][r];
+                    else
+                        vt = (float)vr[m][r >> 1][r & 1];
+                    accp[m][r] = b4[e] * (vt - g4[e] * accp[m][r]);
+                    accp[MT + m][r] *= g4[e];
+                }
+            }
+
         // ---- tree chunks: coupling to the earlier chunks ------------------
         // For t in this chunk and i in an earlier chunk j, B[t, i] U_i and
-        // A[t, i] U_i enter eq. 2 through R and O; with B[t, i] =
+        // A[t, i] U_i enter eq. 2 through R and O, with B[t, i] =
         // beta_t (g_t / g_i) k_t . k_i and A[t, i] = (g_t / g_i) q_t . k_i
-        // (i an ancestor of t), both are g_t times
-        //   sum over ancestors i in chunk j of ((x_t . k_i) / g_i) U_i,  x = k or q,
-        // which is added to [K; Q] S0^T before phase 4 scales by g_t (and
-        // beta_t for R).  Per chunk j: the cross gram [K; Q] K_j^T is masked
-        // and scaled into the K/Q staging area (free once P is done), and its
-        // product with U_j (written by this workgroup one or more chunks ago)
-        // is accumulated on the matrix cores.  The chunk's own K and Q come
-        // from that staging area for the first earlier chunk and from the
-        // cache after it has been overwritten; K_j always from the cache.
+        // (i an ancestor of t).  So after phase 4 the coupling adds
+        //   sum over ancestors i in chunk j of -beta_t (g_t / g_i) (k_t . k_i) U_i  to R,
+        //   sum over ancestors i in chunk j of (g_t / g_i) (q_t . k_i) U_i          to O,
+        // each ratio g_t / g_i <= 1 formed whole.  Per chunk j: the cross
+        // gram [K; Q] K_j^T is masked and scaled into the K/Q staging area
+        // (free once P is done), and its product with U_j (written by this
+        // workgroup one or more chunks ago) is accumulated on the matrix
+        // cores.  The chunk's own K and Q come from that staging area for the
+        // first earlier chunk and from the cache after it has been
+        // overwritten; K_j always from the cache.
         if constexpr (XT) {
             float *Ck = reinterpret_cast<float *>(lds), *Cq = Ck + NP * MS;
             static_assert(2 * NP * MS * 4 <= L::B_OFF, "the coupling blocks fit where K/Q were staged");
@@ -993,13 +1037,26 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                     load_u();
                     if (j == 0) __syncthreads();         // the coupling blocks are written over the staged K/Q
                     const int i = 32 * nt + l32;
-                    const float inv_gi = 1.f / g_all[64 * j + i];   // every node of an earlier chunk is real
+                    const float inv_mi = 1.f / gm_all[64 * j + i];  // every node of an earlier chunk is real
+                    const int ei = ge_all[64 * j + i];
+                    // (rows in runs of four, one 16-byte read of their decays
+                    // each; the barrier keeps the reads from being hoisted)
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int t = 32 * mt + acc_row(r, hg);
-                        const bool a = (anc_all[(base + t) * MASK_WORDS + j] >> i) & 1ull;
-                        Ck[t * MS + i] = a ? gkk[r] * inv_gi : 0.f;
-                        Cq[t * MS + i] = a ? gqk[r] * inv_gi : 0.f;
+                    for (int r4 = 0; r4 < 16; r4 += 4) {
+                        const int t0 = 32 * mt + acc_row(r4, hg);
+                        const f32x4 m4 = *reinterpret_cast<const f32x4 *>(gm_s + t0);
+                        const int4 e4 = *reinterpret_cast<const int4 *>(ge_s + t0);
+                        const f32x4 b4 = *reinterpret_cast<const f32x4 *>(be_s + t0);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int r = r4 + e, t = t0 + e;
+                            const bool a = (anc_all[(base + t) * MASK_WORDS + j] >> i) & 1ull;
+                            const int et = e == 0 ? e4.x : e == 1 ? e4.y : e == 2 ? e4.z : e4.w;
+                            const float ratio = DecayX::ratio(m4[e], et, inv_mi, ei);
+                            Ck[t * MS + i] = a ? -b4[e] * ratio * gkk[r] : 0.f;
+                            Cq[t * MS + i] = a ? gqk[r] * ratio : 0.f;
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
                     }
                 }
                 __syncthreads();
@@ -1024,21 +1081,6 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             }
         }
 
-        // ---- phase 4: R and g P_Q ---------------------------------------------
-#pragma unroll
-        for (int m = 0; m < MT; ++m)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int t = 32 * m + acc_row(r, hg);
-                const float gt = g_s[t];
-                float vt;
-                if constexpr (F32IN)
-                    vt = vr[m][r];
-                else
-                    vt = (float)vr[m][r >> 1][r & 1];
-                accp[m][r] = be_s[t] * (vt - gt * accp[m][r]);
-                accp[MT + m][r] *= gt;
-            }
         // Chain prefill: the Q rows staged in LDS are dead once P is done;
         // K goes there transposed for the state update at the end of the
         // chunk: row j holds K[l][d_k = j] (staged at position kperm(j)) in
@@ -1109,7 +1151,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // the barrier that ends P, whereas beta is still read by the other
         // waves' phase 4 (no barrier orders this write after those reads).
         float *wt_s = reinterpret_cast<float *>(anc_s);
-        if (PRE && wave == 0) wt_s[lane] = lane < N ? g_s[N - 1] / g_s[lane] : 0.f;
+        if (PRE && wave == 0)
+            wt_s[lane] = lane < N ? DecayX::ratio(gm_s[N - 1], ge_s[N - 1], 1.f / gm_s[lane], ge_s[lane]) : 0.f;
         const rsrc_t ru = make_rsrc(PRE ? nullptr : U + (unode0 + base) * D, PRE ? 0 : N * D * 4);
         const rsrc_t ro = make_rsrc(o + node0 * D, N * D * (int)sizeof(In));
         // U leaves while A U runs (rows of padding nodes fall past the end of
@@ -1200,7 +1243,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             // their row order), the A operand from K^T transposed into LDS in
             // the same order; the result rows are this lane's S entries.
             __syncthreads();                             // the weights and K^T, from every wave
-            const float gN = g_s[N - 1];
+            const float gN = DecayX::value(gm_s[N - 1], ge_s[N - 1]);
             bf16x8 ubh[2 * MT], ubl[2 * MT];
 #pragma unroll
             for (int s2 = 0; s2 < 2 * MT; ++s2) {
@@ -1254,12 +1297,17 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 
 namespace {
 
+// Resident workgroups of this kernel variant on the current device, cached
+// per device: the library's only process-wide state.  Every thread that
+// computes it computes the same value, so concurrent first calls may both
+// store it; the relaxed atomics make that race-free.
 template <int NP, bool F32IN, bool FUSE, bool SBF, int MODE = ONE_PASS>
 int resident_grid(int units) {
-    static int per_device[64] = {0};
+    static std::atomic<int> per_device[64];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
-    if (per_device[dev] == 0) {
+    int slots = per_device[dev].load(std::memory_order_relaxed);
+    if (slots == 0) {
         int cus = 0, blocks = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
             cus = 256;
@@ -1267,9 +1315,10 @@ int resident_grid(int units) {
                                                          0) != hipSuccess ||
             blocks <= 0)
             blocks = 1;
-        per_device[dev] = cus * blocks;
+        slots = cus * blocks;
+        per_device[dev].store(slots, std::memory_order_relaxed);
     }
-    return units < per_device[dev] ? units : per_device[dev];
+    return units < slots ? units : slots;
 }
 
 template <int NP, bool F32IN, bool FUSE, bool SBF, int MODE = ONE_PASS>

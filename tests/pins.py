@@ -203,6 +203,64 @@ def pin_closed_form(orc, cases=((0, 2, 1, 4), (2, 2, 2, 16), (3, 1, 2, 64), (4, 
             assert rel(Sc[u], S_ref) < tol, (cfg, u)
 
 
+def pin_closed_form_fp32(orc, cases=((0, 2, 1, 4), (2, 2, 2, 16), (3, 1, 2, 64), (4, 2, 1, 32),
+                                     (3, 1, 1, 200), (1, 1, 1, 150)), tol=1e-6):
+    """The closed form evaluated entirely in float32 against the float64 oracle
+    on the same fp32 inputs: the paper reports about 1e-7 between the two in
+    single precision (Implementation).  The bar is 1e-6, normwise per unit."""
+    for cfg, B, H, N in cases:
+        w = wl.scaled(wl.WORKLOADS[cfg], B=B, H=H, N=N)
+        x = wl.make_inputs(w, seed=12)
+        rng = np.random.default_rng(100 + cfg)
+        S0 = (rng.standard_normal((B * H, w.d_v, w.d_k)) * 0.2).astype(np.float32)
+        U = B * H
+        par_u = np.repeat(x["parent"], H, axis=0)
+        args = [x[n].reshape(U, N, -1) for n in ("q", "k", "v")]
+        al, be = x["alpha"].reshape(U, N), x["beta"].reshape(U, N)
+        o, vt = orc.verify(S0, *args, al, be, par_u)
+        path = np.repeat(x["path"], H, axis=0)
+        plen = np.repeat(x["path_len"], H, axis=0)
+        Sc = orc.commit(S0, args[1], args[2], al, be, par_u, path, plen)
+        for u in range(U):
+            O32, V32 = cf.solve_unit(S0[u], args[0][u], args[1][u], args[2][u], al[u], be[u], par_u[u],
+                                     dtype=np.float32)
+            assert rel(V32, vt[u]) < tol, (cfg, u, rel(V32, vt[u]))
+            assert rel(O32, o[u]) < tol, (cfg, u, rel(O32, o[u]))
+            S32 = cf.commit_unit(S0[u], args[1][u], al[u], par_u[u], V32, list(path[u, :plen[u]]),
+                                 dtype=np.float32)
+            assert rel(S32, Sc[u]) < tol, (cfg, u, rel(S32, Sc[u]))
+
+
+def pin_closed_form_fast_decay(orc, tol=1e-12):
+    """Fast-forgetting gates, alpha in (0.02, 0.5): the cumulative decays of a
+    64-node chain and of a 256-node tree of depth 96 fall far below the
+    smallest float32, and the oracle still equals the paper's closed form
+    (eq. 2 solve, read-out, eq. 3) in float64."""
+    for N, depth, caps, seed in ((64, 64, (1,), 21), (256, 96, (4, 4, 2), 22)):
+        tree = "chain" if caps == (1,) else "tree"
+        w = wl.Workload("fast-decay", 1, 2, N, 32, 32, "f32", tree, depth, caps, (0.02, 0.5), (0.05, 0.95),
+                        8, "chain_depth_0_to_N" if tree == "chain" else "uniform_node")
+        x = wl.make_inputs(w, seed=seed)
+        rng = np.random.default_rng(seed)
+        U = w.units
+        S0 = rng.standard_normal((U, w.d_v, w.d_k)) * 0.2
+        par_u = np.repeat(x["parent"], w.H, axis=0)
+        args = [x[n].reshape(U, N, -1) for n in ("q", "k", "v")]
+        al, be = x["alpha"].reshape(U, N), x["beta"].reshape(U, N)
+        g = cf.cumulative_decay(par_u[0], al[0].astype(np.float64))
+        assert g.min() < 1e-39, "the draw must reach where 1 / g overflows float32"
+        o, vt = orc.verify(S0, *args, al, be, par_u)
+        path = np.repeat(x["path"], w.H, axis=0)
+        plen = np.repeat(x["path_len"], w.H, axis=0)
+        Sc = orc.commit(S0, args[1], args[2], al, be, par_u, path, plen)
+        for u in range(U):
+            O_ref, Vt_ref = cf.solve_unit(S0[u], args[0][u], args[1][u], args[2][u], al[u], be[u], par_u[u])
+            assert rel(vt[u], Vt_ref) < tol, (N, u, rel(vt[u], Vt_ref))
+            assert rel(o[u], O_ref) < tol, (N, u, rel(o[u], O_ref))
+            S_ref = cf.commit_unit(S0[u], args[1][u], al[u], par_u[u], Vt_ref, list(path[u, :plen[u]]))
+            assert rel(Sc[u], S_ref) < tol, (N, u)
+
+
 def pin_commit_reads_out_node_output(orc, seed=5):
     """The committed state of node a, applied to q_a, is o_a (eq. 1 + eq. 3)."""
     rng = np.random.default_rng(seed)
@@ -299,6 +357,6 @@ def pin_rejects_bad_trees(orc):
 
 
 ALL_PINS = [pin_scalar_worked_example, pin_exact_rational, pin_chain_literal, pin_beta_zero,
-            pin_overwrite, pin_brute_force_small_trees, pin_closed_form,
+            pin_overwrite, pin_brute_force_small_trees, pin_closed_form, pin_closed_form_fp32, pin_closed_form_fast_decay,
             pin_commit_reads_out_node_output, pin_non_ancestor_invariance, pin_relabel_invariance,
             pin_multi_round, pin_chain_warmup_matches_tree, pin_rejects_bad_trees]
