@@ -14,8 +14,9 @@ workload (the 4-node fp32 chain, the 35B-shaped chain and tree, and the
 32-node stress tree with the full-state-snapshot comparison: bytes moved and
 speculative memory of both methods), the fused call, the bf16 state, the chain
 prefill, 128-node trees, and the float64 oracle timed on the host's cores as
-a CPU baseline.  The other workloads run first and the headline after them,
-so that its steps run at the clocks the GPU holds under sustained load.
+a CPU baseline.  Every other GPU section runs first and the headline's timed
+steps after them, so that they run at the clocks the GPU holds under
+sustained load; the oracle runs last.
 
   python bench.py [--steps K] [--warmup W] [--workload 0..4] [--gpus 1]
                   [--configs 0,1,2,4 | --no-configs] [--no-snapshot]
@@ -156,21 +157,71 @@ def device_inputs(torch, tw, wl, w, seed):
     return x, d
 
 
+class TimingEvent:
+    """A HIP event used only for timing, created with hipEventDisableSystemFence.
+
+    By default recording an event ends with a system-scope fence, which
+    writes back and invalidates the L2 caches: between two timed launches it
+    adds its own cost to the interval and leaves the next launch cold caches
+    that no serving loop would give it.  HIP offers this flag for events that
+    only measure time; the elapsed times are read after a device-wide
+    synchronize.  The events come from the HIP runtime torch has loaded, so
+    they record on torch's streams."""
+    DISABLE_SYSTEM_FENCE = 0x20000000
+    _hip = None
+
+    @classmethod
+    def runtime(cls):
+        if cls._hip is None:
+            import ctypes
+            path = "libamdhip64.so"
+            for line in open("/proc/self/maps"):
+                if "libamdhip64" in line:
+                    path = line.split()[-1]
+                    break
+            cls._hip = ctypes.CDLL(path)
+        return cls._hip
+
+    def __init__(self):
+        import ctypes
+        self._c = ctypes
+        self.ev = ctypes.c_void_p()
+        rc = self.runtime().hipEventCreateWithFlags(ctypes.byref(self.ev), ctypes.c_uint(self.DISABLE_SYSTEM_FENCE))
+        if rc != 0:
+            raise RuntimeError("hipEventCreateWithFlags failed (%d)" % rc)
+
+    def record(self, stream):
+        rc = self.runtime().hipEventRecord(self.ev, self._c.c_void_p(stream.cuda_stream))
+        if rc != 0:
+            raise RuntimeError("hipEventRecord failed (%d)" % rc)
+
+    def elapsed_time(self, end):
+        ms = self._c.c_float()
+        rc = self.runtime().hipEventElapsedTime(self._c.byref(ms), self.ev, end.ev)
+        if rc != 0:
+            raise RuntimeError("hipEventElapsedTime failed (%d)" % rc)
+        return ms.value
+
+    def __del__(self):
+        if self._hip is not None and self.ev:
+            self._hip.hipEventDestroy(self.ev)
+
+
 def time_steps(torch, launches, steps, warmup, flush=None, stats=None):
     """Run `launches` (a list of callables, one step) W + K times; return the
-    average step time and the average time of each launch (HIP events on the
-    stream the kernels run on).  With `flush`, it runs between steps (outside
-    every launch's events) and the step time is the sum of the launch times.
-    With `stats` (a list), the p10 / p50 / p90 of each launch's times are
-    appended to it."""
+    average step time and the average time of each launch (HIP timing
+    events on the stream the kernels run on).  With `flush`, it runs between
+    steps (outside every launch's events) and the step time is the sum of the
+    launch times.  With `stats` (a list), the p10 / p50 / p90 of each
+    launch's times are appended to it."""
     for _ in range(warmup):
         for f in launches:
             f()
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(launches) + 1)] for _ in range(steps)]
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
+    ev = [[TimingEvent() for _ in range(len(launches) + 1)] for _ in range(steps)]
+    t0 = TimingEvent()
+    t1 = TimingEvent()
     torch.cuda.synchronize()
     t0.record(stream)
     for i in range(steps):
@@ -312,10 +363,11 @@ def snapshot_comparison(torch, tw, acc, w, x, d, o, ms_treewy_step, steps):
     return out
 
 
-def measure_workload(torch, tw, wl, acc, w, args, src_hash, cpu_seconds, snapshot):
-    """One workload's block: verify + commit steps (the headline's step on
-    this workload), the fused call, optionally the snapshot comparison, and
-    the oracle's CPU baseline on a bounded sample."""
+def measure_workload(torch, tw, wl, acc, w, args, src_hash, snapshot):
+    """One workload's block on the GPU: verify + commit steps (the headline's
+    step on this workload), the fused call and optionally the snapshot
+    comparison.  Returns the block and the host inputs (for the oracle's CPU
+    baseline, which runs after all GPU work)."""
     x, d = device_inputs(torch, tw, wl, w, args.seed)
     U = torch.empty((w.B, w.H, w.N, w.d_v), dtype=torch.float32, device="cuda")
     o = torch.empty((w.B, w.H, w.N, w.d_v), dtype=d["q"].dtype, device="cuda")
@@ -358,11 +410,9 @@ def measure_workload(torch, tw, wl, acc, w, args, src_hash, cpu_seconds, snapsho
         block["snapshot_comparison"] = snapshot_comparison(torch, tw, acc, w, x, d, o, ms_step,
                                                            max(3, args.steps // 10))
         log("%s: snapshot baseline %.4f ms/step" % (w.name, block["snapshot_comparison"]["ms_per_step"]))
-    if cpu_seconds > 0:
-        block["cpu_baseline"] = cpu_baseline(w, wl, x, args.seed, cpu_seconds, max_units=2048)
     del d, U, o, S_new, S0_commit
     torch.cuda.empty_cache()
-    return block
+    return block, x
 
 
 def main():
@@ -380,18 +430,25 @@ def main():
     from paper_2608_20961_amd import workload as wl
 
     src_hash = kernel_source_hash()
-    # The other workloads first, each in a block of its own (the 32-node
-    # stress tree with the snapshot comparison it exists for).
-    others = {}
+    # Order: every GPU section first (the other workloads, each in a block of
+    # its own, the 32-node stress tree with the snapshot comparison it exists
+    # for; then the headline workload's other calls), the headline's own W
+    # warmup and K timed steps last among them, and the oracle's CPU
+    # baselines after all GPU work.  So the timed steps run at the clocks the
+    # GPU holds under sustained load, as in a serving loop, rather than in
+    # the first few dozen launches after an idle spell, when verify (not
+    # commit) ran about 10% slower while the clocks settled.
+    others, cpu_jobs = {}, []
     if not args.no_configs:
         for i in [int(c) for c in args.configs.split(",") if c.strip() != ""]:
             if i == args.workload:
                 continue
             wo = wl.WORKLOADS[i]
             log("workload " + wo.describe())
-            others[wo.name] = measure_workload(torch, tw, wl, acc, wo, args, src_hash,
-                                               0 if args.no_cpu_baseline else args.config_cpu_seconds,
-                                               snapshot=not args.no_snapshot and wo.name == "stress-tree32")
+            block, xo = measure_workload(torch, tw, wl, acc, wo, args, src_hash,
+                                         snapshot=not args.no_snapshot and wo.name == "stress-tree32")
+            others[wo.name] = block
+            cpu_jobs.append((block, wo, xo))
 
     w = wl.WORKLOADS[args.workload]
     log("workload " + w.describe() + " (headline)")
@@ -415,35 +472,10 @@ def main():
                          S_new=S_new)
 
     flush = make_flush(torch, acc, w, x["path_len"])
-    dist = []
-    ms_step, (ms_verify, ms_commit) = time_steps(torch, [verify, commit], args.steps, args.warmup, flush, dist)
-    log("timed %d steps: %.4f ms/step (verify %.4f, commit %.4f)" % (args.steps, ms_step, ms_verify, ms_commit))
-    vb = acc.verify_bytes(w)
-    cb = acc.commit_bytes(w, x["path_len"])
-    rf_verify = roofline(vb, ms_verify, load_traffic("verify", w.name, src_hash))
-    rf_commit = roofline(cb, ms_commit, load_traffic("commit", w.name, src_hash))
-    dominant = rf_verify if ms_verify >= ms_commit else rf_commit
+    verify()                                       # U for the fused call's previous round
+    torch.cuda.synchronize()
     nodes = w.B * w.N
-    result = {
-        "metric": METRIC,
-        "value": round(nodes / (ms_step * 1e-3), 1),
-        "unit": "nodes/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 5),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": w.in_dtype, "data": "synthetic",
-        "config": {"workload": w.describe(), "B": w.B, "H": w.H, "N": w.N, "d_k": w.d_k, "d_v": w.d_v,
-                   "step": "treewy_verify + treewy_commit (out of place)", "accumulate": "f32",
-                   "state": "f32", "parallelism": "none (1 GPU)",
-                   "cache_flushed_between_steps": flush is not None,
-                   "measured_after": sorted(others)},
-        "roofline": dict(dominant, kernel="treewy_verify" if dominant is rf_verify else "treewy_commit"),
-        "verify": dict(rf_verify, launch_ms_p10_p50_p90=dist[0], nodes_per_s=round(nodes / (ms_verify * 1e-3), 1),
-                       head_nodes_per_s=round(w.units * w.N / (ms_verify * 1e-3), 1),
-                       useful_tflops=round(acc.verify_flops(w) / (ms_verify * 1e-3) / 1e12, 2)),
-        "commit": dict(rf_commit, launch_ms_p10_p50_p90=dist[1], pct_hbm_peak=round(100 * rf_commit["frac"], 2)),
-        "kernel_source_hash": src_hash,
-    }
+    result = {}
     # Fused: the previous round's commit inside this round's verify
     # (treewy_commit_verify).  The previous round is this round's own draft
     # and paths, so one launch moves commit + verify bytes minus one read of
@@ -461,11 +493,11 @@ def main():
     fb = acc.commit_verify_bytes(w, x["path_len"])
     result["fused_commit_verify"] = dict(
         roofline(fb, ms_fused, load_traffic("commit_verify", w.name, src_hash)),
-        kernel="treewy_commit_verify", nodes_per_s=round(nodes / (ms_fused * 1e-3), 1),
-        speedup_vs_separate_calls=round(ms_step / ms_fused, 3))
+        kernel="treewy_commit_verify", nodes_per_s=round(nodes / (ms_fused * 1e-3), 1))
     del S_fused, o_f, U_f
     # bf16 state storage: the same step with S0 / S_new in bfloat16 (inputs
     # rounded once from the float32 state).
+    ms_step_b = None
     if w.in_dtype == "bf16":
         S0_b = d["S0"].to(torch.bfloat16)
         S0_bc = S0_b.clone()
@@ -495,7 +527,6 @@ def main():
                                load_traffic("commit_bf16state", w.name, src_hash)),
             "fused_commit_verify": roofline(acc.commit_verify_bytes(w, x["path_len"], 2), ms_fb,
                                             load_traffic("commit_verify_bf16state", w.name, src_hash)),
-            "speedup_vs_f32_state": round(ms_step / ms_step_b, 3),
         }
         del S0_b, S0_bc, S_new_b, o_b, U_b, o_f2, U_f2
     # Chain prefill (bf16 tokens, float32 state) at the workload's B x H.
@@ -575,12 +606,53 @@ def main():
     result["speculative_state_bytes"] = {"treewy_U": spec["treewy_U"], "treewy_U_k_alpha": spec["treewy_U_k_alpha"],
                                          "snapshot_states": spec["snapshot_states"]}
     if not args.no_snapshot:
-        result["snapshot_baseline"] = snapshot_comparison(torch, tw, acc, w, x, d, o, ms_step,
-                                                          max(3, args.steps // 10))
+        result["snapshot_baseline"] = snapshot_comparison(torch, tw, acc, w, x, d, o, 1.0, max(3, args.steps // 10))
         log("snapshot baseline: %.4f ms/step" % result["snapshot_baseline"]["ms_per_step"])
+
+    # ---- the headline: W warmup steps, then exactly K timed steps ------------
+    dist = []
+    ms_step, (ms_verify, ms_commit) = time_steps(torch, [verify, commit], args.steps, args.warmup, flush, dist)
+    log("timed %d steps: %.4f ms/step (verify %.4f, commit %.4f)" % (args.steps, ms_step, ms_verify, ms_commit))
+    vb = acc.verify_bytes(w)
+    cb = acc.commit_bytes(w, x["path_len"])
+    rf_verify = roofline(vb, ms_verify, load_traffic("verify", w.name, src_hash))
+    rf_commit = roofline(cb, ms_commit, load_traffic("commit", w.name, src_hash))
+    dominant = rf_verify if ms_verify >= ms_commit else rf_commit
+    head = {
+        "metric": METRIC,
+        "value": round(nodes / (ms_step * 1e-3), 1),
+        "unit": "nodes/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": w.in_dtype, "data": "synthetic",
+        "config": {"workload": w.describe(), "B": w.B, "H": w.H, "N": w.N, "d_k": w.d_k, "d_v": w.d_v,
+                   "step": "treewy_verify + treewy_commit (out of place)", "accumulate": "f32",
+                   "state": "f32", "parallelism": "none (1 GPU)",
+                   "cache_flushed_between_steps": flush is not None,
+                   "timed_after": "the other workloads' blocks and this workload's other sections"},
+        "roofline": dict(dominant, kernel="treewy_verify" if dominant is rf_verify else "treewy_commit"),
+        "verify": dict(rf_verify, launch_ms_p10_p50_p90=dist[0], nodes_per_s=round(nodes / (ms_verify * 1e-3), 1),
+                       head_nodes_per_s=round(w.units * w.N / (ms_verify * 1e-3), 1),
+                       useful_tflops=round(acc.verify_flops(w) / (ms_verify * 1e-3) / 1e12, 2)),
+        "commit": dict(rf_commit, launch_ms_p10_p50_p90=dist[1], pct_hbm_peak=round(100 * rf_commit["frac"], 2)),
+        "kernel_source_hash": src_hash,
+    }
+    result = dict(head, **result)
+    result["fused_commit_verify"]["speedup_vs_separate_calls"] = round(ms_step / ms_fused, 3)
+    if ms_step_b is not None:
+        result["bf16_state"]["speedup_vs_f32_state"] = round(ms_step / ms_step_b, 3)
+    if "snapshot_baseline" in result:
+        sb = result["snapshot_baseline"]
+        sb["treewy_speedup"] = round(sb["ms_per_step"] / ms_step, 2)
     if others:
         result["configs"] = others
+
+    # ---- CPU baselines (after all GPU work) ---------------------------------
     if not args.no_cpu_baseline:
+        for block, wo, xo in cpu_jobs:
+            log("cpu baseline (oracle), %s ..." % wo.name)
+            block["cpu_baseline"] = cpu_baseline(wo, wl, xo, args.seed, args.config_cpu_seconds, max_units=2048)
         log("cpu baseline (oracle) ...")
         result["cpu_baseline"] = cpu_baseline(w, wl, x, args.seed, args.cpu_seconds)
     print(json.dumps(result), flush=True)
