@@ -133,14 +133,13 @@ def copy_calibration(torch):
     print(json.dumps({"copy_calibration_bytes_each_way": 4 * n, "launches": 5}), flush=True)
 
 
-def device_inputs(torch, tw, wl, w, seed):
-    """Seeded inputs on the device; S0 made on the device by the library's
-    chain prefill over the workload's warm-up tokens in float32 (the float32
-    kernels, so a profile's statistics for the timed bf16 kernels cover only
-    the timed launches)."""
+def device_inputs(torch, tw, wl, w, seed, x):
+    """The seeded host inputs `x` on the device; S0 made on the device by the
+    library's chain prefill over the workload's warm-up tokens in float32
+    (the float32 kernels, so a profile's statistics for the timed bf16
+    kernels cover only the timed launches)."""
     dev = torch.device("cuda:0")
     dt = torch.bfloat16 if w.in_dtype == "bf16" else torch.float32
-    x = wl.make_inputs(w, seed=seed)
 
     def put(a, dtype):
         return torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dtype)
@@ -363,12 +362,11 @@ def snapshot_comparison(torch, tw, acc, w, x, d, o, ms_treewy_step, steps):
     return out
 
 
-def measure_workload(torch, tw, wl, acc, w, args, src_hash, snapshot):
+def measure_workload(torch, tw, wl, acc, w, x, d, args, src_hash, snapshot):
     """One workload's block on the GPU: verify + commit steps (the headline's
     step on this workload), the fused call and optionally the snapshot
-    comparison.  Returns the block and the host inputs (for the oracle's CPU
-    baseline, which runs after all GPU work)."""
-    x, d = device_inputs(torch, tw, wl, w, args.seed)
+    comparison, on the host inputs `x` already resident on the device as `d`.
+    Returns the block (the oracle's CPU baseline runs after all GPU work)."""
     U = torch.empty((w.B, w.H, w.N, w.d_v), dtype=torch.float32, device="cuda")
     o = torch.empty((w.B, w.H, w.N, w.d_v), dtype=d["q"].dtype, device="cuda")
     S_new = torch.empty_like(d["S0"])
@@ -412,7 +410,7 @@ def measure_workload(torch, tw, wl, acc, w, args, src_hash, snapshot):
         log("%s: snapshot baseline %.4f ms/step" % (w.name, block["snapshot_comparison"]["ms_per_step"]))
     del d, U, o, S_new, S0_commit
     torch.cuda.empty_cache()
-    return block, x
+    return block
 
 
 def main():
@@ -430,30 +428,51 @@ def main():
     from paper_2608_20961_amd import workload as wl
 
     src_hash = kernel_source_hash()
-    # Order: every GPU section first (the other workloads, each in a block of
-    # its own, the 32-node stress tree with the snapshot comparison it exists
-    # for; then the headline workload's other calls), the headline's own W
-    # warmup and K timed steps last among them, and the oracle's CPU
-    # baselines after all GPU work.  So the timed steps run at the clocks the
-    # GPU holds under sustained load, as in a serving loop, rather than in
-    # the first few dozen launches after an idle spell, when verify (not
-    # commit) ran about 10% slower while the clocks settled.
-    others, cpu_jobs = {}, []
-    if not args.no_configs:
-        for i in [int(c) for c in args.configs.split(",") if c.strip() != ""]:
-            if i == args.workload:
-                continue
-            wo = wl.WORKLOADS[i]
-            log("workload " + wo.describe())
-            block, xo = measure_workload(torch, tw, wl, acc, wo, args, src_hash,
-                                         snapshot=not args.no_snapshot and wo.name == "stress-tree32")
-            others[wo.name] = block
-            cpu_jobs.append((block, wo, xo))
-
+    # Order.  Every workload's inputs are drawn on the host and made resident
+    # on the device (with its S0) first.  Then the GPU sections run back to
+    # back: the other workloads, each in a block of its own (the 32-node
+    # stress tree with the snapshot comparison it exists for), the headline
+    # workload's other calls, and last the headline's own W warmup and K
+    # timed steps.  The oracle's CPU baselines run after all GPU work.  The
+    # GPU's compute clock falls within milliseconds of idling (host work,
+    # host-to-device copies) and takes about 10 ms of sustained work to come
+    # back, and verify and the fused call (not commit) ran about 10% slower
+    # in the launches after such an idle spell; this order times every
+    # section at the clocks the GPU holds under sustained load, as in a
+    # serving loop.
     w = wl.WORKLOADS[args.workload]
-    log("workload " + w.describe() + " (headline)")
-    x, d = device_inputs(torch, tw, wl, w, args.seed)
+    ids = [] if args.no_configs else [int(c) for c in args.configs.split(",") if c.strip() != ""]
+    ids = [i for i in ids if i != args.workload]
+    hosts = {i: wl.make_inputs(wl.WORKLOADS[i], seed=args.seed) for i in ids + [args.workload]}
+    big = not args.no_big_tree and w.in_dtype == "bf16" and w.B == wl.BIG_TREE.B and w.H == wl.BIG_TREE.H
+    xb = wl.make_inputs(wl.BIG_TREE, seed=args.seed) if big else None
+    tok = wl.acceptance_tokens(hosts[args.workload]["parent"], seed=args.seed, vocab=4, plant=True)
+    log("host inputs drawn")
+    devs = {i: device_inputs(torch, tw, wl, wl.WORKLOADS[i], args.seed, hosts[i])[1] for i in ids + [args.workload]}
+    Tp = args.prefill_tokens if w.in_dtype == "bf16" else 0
+    if Tp > 0:
+        kp, vp, ap, bp = wl.warmup_chunk_torch(w, args.seed, 1, Tp, "cuda", torch.bfloat16)
+        qp = wl.warmup_chunk_torch(w, args.seed, 2, Tp, "cuda", torch.bfloat16)[0]
+    if big:
+        wb = wl.BIG_TREE
+        put = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to("cuda").to(dt)
+        bq, bk, bv = (put(xb[n], torch.bfloat16) for n in ("q", "k", "v"))
+        ba, bb = put(xb["alpha"], torch.float32), put(xb["beta"], torch.float32)
+        bpar, bpath, bplen = (put(xb[n], torch.int32) for n in ("parent", "path", "path_len"))
+    t_d, t_t, t_r = (torch.from_numpy(tok[n]).to("cuda") for n in ("draft", "target", "root"))
+    torch.cuda.synchronize()
     log("inputs resident, S0 warmed on the device")
+    others, cpu_jobs = {}, []
+    for i in ids:
+        wo = wl.WORKLOADS[i]
+        log("workload " + wo.describe())
+        block = measure_workload(torch, tw, wl, acc, wo, hosts[i], devs.pop(i), args, src_hash,
+                                 snapshot=not args.no_snapshot and wo.name == "stress-tree32")
+        others[wo.name] = block
+        cpu_jobs.append((block, wo, hosts[i]))
+
+    log("workload " + w.describe() + " (headline)")
+    x, d = hosts[args.workload], devs.pop(args.workload)
     U = torch.empty((w.B, w.H, w.N, w.d_v), dtype=torch.float32, device="cuda")
     o = torch.empty((w.B, w.H, w.N, w.d_v), dtype=d["q"].dtype, device="cuda")
     S_new = torch.empty_like(d["S0"])
@@ -530,10 +549,7 @@ def main():
         }
         del S0_b, S0_bc, S_new_b, o_b, U_b, o_f2, U_f2
     # Chain prefill (bf16 tokens, float32 state) at the workload's B x H.
-    Tp = args.prefill_tokens
-    if Tp > 0 and w.in_dtype == "bf16":
-        kp, vp, ap, bp = wl.warmup_chunk_torch(w, args.seed, 1, Tp, "cuda", torch.bfloat16)
-        qp = wl.warmup_chunk_torch(w, args.seed, 2, Tp, "cuda", torch.bfloat16)[0]
+    if Tp > 0:
         S_p = torch.empty_like(d["S0"])
         o_p = torch.empty_like(vp)
 
@@ -548,13 +564,7 @@ def main():
         del kp, vp, ap, bp, qp, S_p, o_p
     # Trees past one 64-node chunk: 128-node trees at the same layer shape
     # (verify walks two chunks per unit; commit follows paths up to 16 long).
-    if not args.no_big_tree and w.in_dtype == "bf16" and w.B == wl.BIG_TREE.B and w.H == wl.BIG_TREE.H:
-        wb = wl.BIG_TREE
-        xb = wl.make_inputs(wb, seed=args.seed)
-        put = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to("cuda").to(dt)
-        bq, bk, bv = (put(xb[n], torch.bfloat16) for n in ("q", "k", "v"))
-        ba, bb = put(xb["alpha"], torch.float32), put(xb["beta"], torch.float32)
-        bpar, bpath, bplen = (put(xb[n], torch.int32) for n in ("parent", "path", "path_len"))
+    if big:
         o_b = torch.empty((wb.B, wb.H, wb.N, wb.d_v), dtype=torch.bfloat16, device="cuda")
         U_b = torch.empty((wb.B, wb.H, wb.N, wb.d_v), dtype=torch.float32, device="cuda")
         S_nb = torch.empty_like(d["S0"])
@@ -581,8 +591,6 @@ def main():
         del bq, bk, bv, ba, bb, bpar, bpath, bplen, o_b, U_b, S_nb
     # Greedy acceptance on the device (tokens: vocabulary of 4, the target
     # agreeing with the drafter along one planted chain per sequence).
-    tok = wl.acceptance_tokens(x["parent"], seed=args.seed, vocab=4, plant=True)
-    t_d, t_t, t_r = (torch.from_numpy(tok[n]).to("cuda") for n in ("draft", "target", "root"))
     acc_path = torch.empty((w.B, w.max_depth), dtype=torch.int32, device="cuda")
     acc_len = torch.empty((w.B,), dtype=torch.int32, device="cuda")
     acc_bonus = torch.empty((w.B,), dtype=torch.int32, device="cuda")
