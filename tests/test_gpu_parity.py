@@ -296,3 +296,30 @@ def test_snapshot_baseline(tw, cfg, dtype):
     for t in range(w.N):
         assert_close("snapshot S_%d" % t, got[:, t], states[:, t], tol)
     assert_close("snapshot commit", units_of(S_new, w, case.check), S_ref, tol)
+
+
+def test_snapshot_baseline_full_size_sampled(tw):
+    """The snapshot baseline at the launch the benchmark times (the 32-node
+    stress tree, B = 256, H = 64: 32 GiB of snapshots), checked on 16 sampled
+    units: every node's output and state, and the committed state."""
+    w = wl.WORKLOADS[4]
+    case = Case(w, seed=16, cfg_key=4, check_units=wl.sample_units(w, 16))
+    say("[gpu] snapshot baseline, full size: %s" % w.describe())
+    d = case.device()
+    snaps = torch.empty((w.B, w.H, w.N, w.d_v, w.d_k), dtype=torch.float32, device=DEV)
+    o, snaps = tw.treewy_snapshot_verify(d["S0"], d["q"], d["k"], d["v"], d["alpha"], d["beta"], d["parent"],
+                                         snapshots=snaps)
+    acc = torch.tensor([int(case.x["path"][b, case.x["path_len"][b] - 1]) if case.x["path_len"][b] else -1
+                        for b in range(w.B)], dtype=torch.int32, device=DEV)
+    S_new = tw.treewy_snapshot_commit(d["S0"], snaps, acc)
+    torch.cuda.synchronize()
+    sel = torch.from_numpy(case.check).to(DEV)
+    got = snaps.reshape(w.units, w.N, w.d_v, w.d_k).index_select(0, sel).cpu().numpy()
+    del snaps
+    torch.cuda.empty_cache()
+    o_ref, _, states, S_ref = case.oracle(states=True)
+    tol = TOL[w.in_dtype]
+    eo = assert_close("snapshot o", units_of(o, w, case.check), o_ref, tol)
+    es = max(assert_close("snapshot S_%d" % t, got[:, t], states[:, t], tol) for t in range(w.N))
+    ec = assert_close("snapshot commit", units_of(S_new, w, case.check), S_ref, tol)
+    say("[gpu] snapshot full size: max rel err o %.2e states %.2e commit %.2e" % (eo, es, ec))
