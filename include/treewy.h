@@ -15,11 +15,8 @@
  * Conventions shared by every call:
  *  - All tensor pointers are DEVICE pointers to row-major, contiguous arrays
  *    whose base address is 16-byte aligned.  The caller allocates and owns
- *    every buffer and the library allocates nothing.  Its only process-wide
- *    state is a per-device cache of how many workgroups of each kernel fit on
- *    the GPU at once, filled on first use with relaxed atomic stores of a
- *    value every caller computes alike; calls are re-entrant and may come
- *    from several host threads.
+ *    every buffer; the library allocates nothing and keeps no state between
+ *    calls, so calls are re-entrant and may come from several host threads.
  *  - Sizes supported: d_k == d_v == 128, 0 <= N <= 256 (N = 0 is an empty
  *    draft), 0 <= L_max <= 256, B * H < 2^31; the fused call and the
  *    snapshot baseline take N, N_prev, L_max <= 64.  Other sizes return

@@ -1,6 +1,6 @@
-// treewy_verify kernel: one workgroup (four wave64s) per (sequence, head) unit
-// at a time; the grid is sized to the resident capacity of the GPU and every
-// workgroup walks a strided list of units.
+// treewy_verify kernel: one workgroup (four wave64s) per (sequence, head)
+// unit, launched one workgroup per unit (the kernel also walks a strided list
+// of units when the grid is smaller).
 //
 // The method (Method, eq. 2 and the read-out of the same solve), per unit:
 //   g_t    = product of alpha over t and its ancestors
@@ -51,8 +51,6 @@
 // than 64 nodes, each chunk using S0 (read again per chunk for an fp32
 // state, kept in registers for a bf16 one) and coupled to the pseudo-values
 // of its ancestors in earlier chunks before its own solve.
-#include <atomic>
-
 #include "device.h"
 #include "launch.h"
 
@@ -1297,37 +1295,16 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 
 namespace {
 
-// Resident workgroups of this kernel variant on the current device, cached
-// per device: the library's only process-wide state.  Every thread that
-// computes it computes the same value, so concurrent first calls may both
-// store it; the relaxed atomics make that race-free.
-template <int NP, bool F32IN, bool FUSE, bool SBF, int MODE = ONE_PASS>
-int resident_grid(int units) {
-    static std::atomic<int> per_device[64];
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
-    int slots = per_device[dev].load(std::memory_order_relaxed);
-    if (slots == 0) {
-        int cus = 0, blocks = 0;
-        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-            cus = 256;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, verify_kernel<NP, F32IN, FUSE, SBF, MODE>, THREADS,
-                                                         0) != hipSuccess ||
-            blocks <= 0)
-            blocks = 1;
-        slots = cus * blocks;
-        per_device[dev].store(slots, std::memory_order_relaxed);
-    }
-    return units < slots ? units : slots;
-}
-
 template <int NP, bool F32IN, bool FUSE, bool SBF, int MODE = ONE_PASS>
 hipError_t launch(const void *S0, const void *q, const void *k, const void *v, const float *alpha,
                   const float *beta, const int32_t *parent, int N, int in_stride, int u_stride, int B, int H,
                   void *o, float *U, int32_t *err, const CommitArgs &cm, hipStream_t stream) {
+    // One workgroup per unit: the hardware hands each CU a new unit as soon
+    // as one of its workgroups retires.  (Resident workgroups walking a fixed
+    // strided list of units finished up to 13% apart, the launch waiting for
+    // the slowest; the kernel still accepts any grid size.)
     const int units = B * H;
-    hipLaunchKernelGGL((verify_kernel<NP, F32IN, FUSE, SBF, MODE>),
-                       dim3((unsigned)resident_grid<NP, F32IN, FUSE, SBF, MODE>(units)), dim3(THREADS), 0, stream,
+    hipLaunchKernelGGL((verify_kernel<NP, F32IN, FUSE, SBF, MODE>), dim3((unsigned)units), dim3(THREADS), 0, stream,
                        S0, q, k, v, alpha, beta, parent, N, in_stride, u_stride, H, units, o, U, err, cm);
     return hipGetLastError();
 }
