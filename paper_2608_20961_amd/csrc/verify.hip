@@ -1,6 +1,5 @@
 // treewy_verify kernel: one workgroup (four wave64s) per (sequence, head)
-// unit, launched one workgroup per unit (the kernel also walks a strided list
-// of units when the grid is smaller).
+// unit, launched one workgroup per unit.
 //
 // The method (Method, eq. 2 and the read-out of the same solve), per unit:
 //   g_t    = product of alpha over t and its ancestors
@@ -95,13 +94,12 @@ struct VerifyLds {
     static constexpr bool V_IN_BA = V_BYTES <= 2 * M_BYTES;  // V staged over B and A before the gram
     static constexpr int V_OFF = V_IN_BA ? B_OFF : END_O;
     static constexpr int BASE_BYTES = V_IN_BA ? END_O : END_O + V_BYTES;
-    // Fused commit: the accepted path (node, weight, then its length and g_a)
-    // in two buffers, this unit's and the next one's, and CL path rows at a
-    // time, transposed: k as [d_k][CL], w U as [d_v][CL].
+    // Fused commit: the accepted path (node, weight, then its length and g_a),
+    // and CL path rows at a time, transposed: k as [d_k][CL], w U as [d_v][CL].
     static constexpr int CL = 8;
     static constexpr int META_BYTES = 64 * 4 + 64 * 4 + 16;
     static constexpr int META_OFF = BASE_BYTES;
-    static constexpr int KPT_OFF = META_OFF + 2 * META_BYTES;
+    static constexpr int KPT_OFF = META_OFF + META_BYTES;
     static constexpr int UWT_OFF = KPT_OFF + D * CL * (F32IN ? 4 : 2);
     static constexpr int BYTES = FUSE ? UWT_OFF + D * CL * 4 : BASE_BYTES;
     // Trees of more than 64 nodes, walked in chunks of 64: every node's
@@ -374,16 +372,11 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             if (!ok) flag_error(err, bb, TREEWY_FLAG_BAD_PATH);
         }
     };
-    int u = blockIdx.x;
-    if constexpr (FUSE) {                                // path of the first unit
-        if (wave == 3 && u < units) {
-            const int lane = threadIdx.x & 63;
-            rd.issue_path(cm, u, u / H, lane);
-            path_meta(u, 0, lane);
-        }
-        __syncthreads();
-    }
-    for (int buf = 0; u < units; u += gridDim.x, buf ^= 1) {
+    // One workgroup per unit (the launch is one workgroup per unit).
+    const int u = blockIdx.x;
+    if (u >= units) return;                              // (uniform across the workgroup)
+    constexpr int buf = 0;                               // the fused call's path metadata buffer
+    {
         const int b = u / H;
         // Chunked modes: the unit's nodes in chunks of 64 (the chain prefill
         // keeps the state in registers from one chunk to the next).
@@ -448,30 +441,36 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             *reinterpret_cast<f32x4 *>(UwT + sc * CL + 4 * sh) = *reinterpret_cast<const f32x4 *>(ux);
         };
 
-        // Reads, in the order they are needed.  Fused: wave 3 first fetches
-        // the next unit's path (it turns it into metadata in phase 1), then
-        // every thread its share of this unit's first CL path rows (their
-        // nodes were found one unit ahead), then the unit's own reads.
+        // Reads, in the order they are needed.  Fused: the unit's K/Q/V
+        // first; then the previous round's accepted path, which wave 3 turns
+        // into metadata; then every thread's share of its first CL path rows;
+        // S_old last.  Vector-memory counters retire in order, so the wait for
+        // the path rows (phase 1) covers K/Q/V, which staging needs anyway,
+        // but not S_old, which only P needs.
         int clen = 0;
         float ga = 1.f;
         PathPiece cp;
-        const int u_next = u + (int)gridDim.x;
-        const bool has_next = (long long)u + gridDim.x < units;
-        if constexpr (FUSE) {
-            clen = *meta_len(buf);
-            ga = *meta_ga(buf);
-            if (wave == 3 && has_next) rd.issue_path(cm, u_next, u_next / H, lane);
-            stage_load(0, clen, cp);
-        }
         // (one workgroup per CU only: at two, the other workgroup hides the loads)
         constexpr bool AHEAD = PRE && F32IN;             // the chain prefill fetches the next chunk early
         // Tree chunks read S0 again for every chunk, except with a bf16 state:
         // its 32 registers stay live from the first chunk without spills (the
         // fp32 state's 64 do not fit beside the coupling).
         constexpr bool RELOAD_STATE = XT && !SBF;
-        if (!AHEAD || chunk == 0)                        // (then later chunks were fetched one chunk ahead)
+        if constexpr (FUSE) {
+            rd.template issue<STREAM>(S0, q, k, v, alpha, beta, prow, u, N, node0, false, tid, lane, wave, hg, col);
+            if (wave == 3) {
+                rd.issue_path(cm, u, b, lane);
+                path_meta(u, buf, lane);
+            }
+            __syncthreads();                             // the path metadata, from wave 3
+            clen = *meta_len(buf);
+            ga = *meta_ga(buf);
+            stage_load(0, clen, cp);
+            rd.issue_state(S0, u, hg, col);
+        } else if (!AHEAD || chunk == 0) {               // (then later chunks were fetched one chunk ahead)
             rd.template issue<XT ? CACHED : STREAM>(S0, q, k, v, alpha, beta, prow, u, N, node0,
                                                     chunk == 0 || RELOAD_STATE, tid, lane, wave, hg, col);
+        }
 
         // ---- phase 1: ancestors and cumulative decay by pointer jumping ----
         // Lane t of wave 0 keeps (ptr, prod, mask): ptr an ancestor of t (or
@@ -538,12 +537,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             const bool shallow = !__any(__popcll(mask) > FAST);
             if (lane == 0) *shallow_s = shallow ? 1 : 0;
         }
-        // Fused: the path rows (first in line) go to LDS, and wave 3, idle
-        // here, turns the next unit's path into metadata.
-        if constexpr (FUSE) {
-            stage_store(0, cp);
-            if (wave == 3 && has_next) path_meta(u_next, buf ^ 1, lane);
-        }
+        // Fused: the path rows go to LDS.
+        if constexpr (FUSE) stage_store(0, cp);
         // K and Q into LDS as bf16 (hi/lo for fp32 input), padding rows zero,
         // with the d_k order permuted by kperm (see UnitReads::kperm).
         auto stage_x = [&](__bf16 *xh, __bf16 *xl, int r, int c, const uint4 &val) {
@@ -1282,7 +1277,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // (Tree chunks read this chunk's U rows back in later chunks: the
         // barrier makes a workgroup's global stores visible to its own later
         // loads, with no cache maintenance at workgroup scope.)
-        __syncthreads();                                 // LDS is rewritten by the next unit / chunk
+        __syncthreads();                                 // LDS is rewritten by the next chunk
         }                                                // chunk
         if constexpr (PRE) {                             // the state after the unit's last token
             const int lane = threadIdx.x & 63;
@@ -1302,7 +1297,7 @@ hipError_t launch(const void *S0, const void *q, const void *k, const void *v, c
     // One workgroup per unit: the hardware hands each CU a new unit as soon
     // as one of its workgroups retires.  (Resident workgroups walking a fixed
     // strided list of units finished up to 13% apart, the launch waiting for
-    // the slowest; the kernel still accepts any grid size.)
+    // the slowest.)
     const int units = B * H;
     hipLaunchKernelGGL((verify_kernel<NP, F32IN, FUSE, SBF, MODE>), dim3((unsigned)units), dim3(THREADS), 0, stream,
                        S0, q, k, v, alpha, beta, parent, N, in_stride, u_stride, H, units, o, U, err, cm);
