@@ -598,72 +598,6 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             }
         }
 
-        // ---- phase 2: masked, decay-weighted gram tiles (lower triangle) --
-        //   B[t,i] = beta_t (g_t/g_i) (k_t . k_i)  for i a strict ancestor of t
-        //   A[t,i] = (g_t/g_i) (q_t . k_i)          for i ancestor-or-self of t
-        // Every entry of B and A is written: the upper tile as zeros.
-        constexpr int NPAIRS = MT * (MT + 1) / 2;
-        if (wave < NPAIRS) {
-            const int mt = wave == 0 ? 0 : 1;
-            const int nt = wave == 2 ? 1 : 0;
-            f32x16 gkk = {}, gqk = {};
-            const __bf16 *ak_row = Xh + (32 * mt + l32) * XS + 8 * hg;
-            const __bf16 *aq_row = Xh + (NP + 32 * mt + l32) * XS + 8 * hg;
-            const __bf16 *bk_row = Xh + (32 * nt + l32) * XS + 8 * hg;
-#pragma unroll 2
-            for (int s = 0; s < 8; ++s) {
-                const bf16x8 ak = *reinterpret_cast<const bf16x8 *>(ak_row + 16 * s);
-                const bf16x8 aq = *reinterpret_cast<const bf16x8 *>(aq_row + 16 * s);
-                const bf16x8 bk = *reinterpret_cast<const bf16x8 *>(bk_row + 16 * s);
-                gkk = mma(ak, bk, gkk);
-                gqk = mma(aq, bk, gqk);
-                if constexpr (F32IN) {
-                    const ptrdiff_t lo = Xl - Xh;
-                    const bf16x8 akl = *reinterpret_cast<const bf16x8 *>(ak_row + lo + 16 * s);
-                    const bf16x8 aql = *reinterpret_cast<const bf16x8 *>(aq_row + lo + 16 * s);
-                    const bf16x8 bkl = *reinterpret_cast<const bf16x8 *>(bk_row + lo + 16 * s);
-                    gkk = mma(ak, bkl, gkk);
-                    gkk = mma(akl, bk, gkk);
-                    gqk = mma(aq, bkl, gqk);
-                    gqk = mma(aql, bk, gqk);
-                }
-            }
-            const int ci = 32 * nt + l32;
-            const float inv_mi = 1.f / gm_s[ci];
-            const int ei = ge_s[ci];
-            // The accumulator rows come in runs of four consecutive nodes, so
-            // their decays, betas and ancestor masks arrive as 16-byte LDS
-            // broadcasts; bit ci of a mask sits in word nt of the row's u64.
-#pragma unroll
-            for (int r4 = 0; r4 < 16; r4 += 4) {
-                const int t0 = 32 * mt + acc_row(r4, hg);      // rows t0 .. t0 + 3
-                const f32x4 g4 = *reinterpret_cast<const f32x4 *>(gm_s + t0);
-                const int4 e4 = *reinterpret_cast<const int4 *>(ge_s + t0);
-                const f32x4 b4 = *reinterpret_cast<const f32x4 *>(be_s + t0);
-                const uint4 m01 = *reinterpret_cast<const uint4 *>(anc_s + t0);
-                const uint4 m23 = *reinterpret_cast<const uint4 *>(anc_s + t0 + 2);
-                const uint32_t w[4] = {nt ? m01.y : m01.x, nt ? m01.w : m01.z,
-                                       nt ? m23.y : m23.x, nt ? m23.w : m23.z};
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int r = r4 + e, t = t0 + e;
-                    const bool strict = (w[e] >> l32) & 1u;
-                    const int et = e == 0 ? e4.x : e == 1 ? e4.y : e == 2 ? e4.z : e4.w;
-                    const float ratio = strict ? DecayX::ratio(g4[e], et, inv_mi, ei) : (ci == t ? 1.f : 0.f);
-                    Bm[t * MS + ci] = strict ? b4[e] * ratio * gkk[r] : 0.f;
-                    Am[t * MS + ci] = ratio * gqk[r];
-                }
-            }
-        } else if (MT == 2 && wave == 3) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int t = acc_row(r, hg);
-                Bm[t * MS + 32 + l32] = 0.f;
-                Am[t * MS + 32 + l32] = 0.f;
-            }
-        }
-
-        __syncthreads();
         // ---- fused commit: S0 = g_a S_old + sum_l w_l U_prev[a_l] k_prev[a_l]^T
         // The rank-L term runs on the matrix cores as (K_path^T)(w U_path)
         // over 32-row blocks of d_k; its accumulator rows are exactly the d_k
@@ -700,6 +634,161 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             return acc;
         };
         const bool upd_in_p = FUSE && clen > 0 && clen <= CL;
+        const rsrc_t rn = make_rsrc(FUSE ? static_cast<char *>(cm.S_new) + (size_t)u * D * D * SB : nullptr,
+                                    FUSE ? D * D * SB : 0);
+        // ---- P = [K; Q] S0^T for this wave's 32 columns (phase 3) -----------
+        // The A operands (rows of [K; Q] in LDS) are double-buffered one
+        // K-step ahead; the scheduling barriers keep the compiler from
+        // hoisting every step's operands at once.
+        // With 32 rows, waves 2 and 3 have no gram work and run P during the gram.
+        constexpr bool EARLY_P = NP == 32 && !FUSE;
+        f32x16 accp[2 * MT];
+        auto run_p = [&]() {
+#pragma unroll
+        for (int m = 0; m < 2 * MT; ++m) accp[m] = f32x16{};
+            // (one buffer in the fused variant, whose update block needs the registers)
+            constexpr int NBUF = FUSE ? 1 : 2;
+            bf16x8 afr[NBUF][2 * MT], alo[NBUF][2 * MT];
+            auto load_a = [&](int buf, int s) {
+#pragma unroll
+                for (int m = 0; m < 2 * MT; ++m) {
+                    const __bf16 *arow = Xh + (32 * m + l32) * XS + 16 * s + 8 * hg;
+                    afr[buf][m] = *reinterpret_cast<const bf16x8 *>(arow);
+                    if constexpr (F32IN) alo[buf][m] = *reinterpret_cast<const bf16x8 *>(arow + (Xl - Xh));
+                }
+            };
+            if (NBUF == 2) load_a(0, 0);
+            f32x16 dcur = {};
+#pragma unroll
+            for (int s = 0; s < 8; ++s) {
+                if (NBUF == 1)
+                    load_a(0, s);
+                else if (s < 7)
+                    load_a((s + 1) & 1, s + 1);
+                if constexpr (FUSE) {                    // S0 pieces of step s: commit update
+                    if (upd_in_p) {
+                        if ((s & 1) == 0) dcur = rank_block(s >> 1, f32x16{});
+#pragma unroll
+                        for (int h = 0; h < 2; ++h) {
+                            f32x4 x = rd.sget(s, h);
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) x[i] = fmaf(ga, x[i], dcur[8 * (s & 1) + 4 * h + i]);
+                            rd.sset(s, h, x);                   // a bf16 state is rounded here, then used
+                        }
+                    }
+                }
+                bf16x8 bh, bl;
+                if constexpr (SBF) {                     // a bf16 state is exact on the matrix cores
+                    bh = __builtin_bit_cast(bf16x8, make_uint4(rd.s0[s][0].x, rd.s0[s][0].y, rd.s0[s][1].x,
+                                                               rd.s0[s][1].y));
+                } else {
+                    float sv[8];
+                    *reinterpret_cast<f32x4 *>(sv) = rd.s0[s][0];
+                    *reinterpret_cast<f32x4 *>(sv + 4) = rd.s0[s][1];
+                    split8(sv, bh, bl);
+                }
+#pragma unroll
+                for (int m = 0; m < 2 * MT; ++m) {
+                    accp[m] = mma(afr[s % NBUF][m], bh, accp[m]);
+                    if constexpr (!SBF) accp[m] = mma(afr[s % NBUF][m], bl, accp[m]);
+                    if constexpr (F32IN) accp[m] = mma(alo[s % NBUF][m], bh, accp[m]);
+                }
+                // S_new leaves line by line once the steps that hold a line are done.
+                if constexpr (FUSE) {
+                    if (s % Reads::LINE_STEPS == Reads::LINE_STEPS - 1) rd.store_state_line(rn, s / Reads::LINE_STEPS, wave, lane);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+
+        // ---- phase 2: masked, decay-weighted gram tiles (lower triangle) --
+        //   B[t,i] = beta_t (g_t/g_i) (k_t . k_i)  for i a strict ancestor of t
+        //   A[t,i] = (g_t/g_i) (q_t . k_i)          for i ancestor-or-self of t
+        // Every entry of B and A is written: the upper tile as zeros.
+        constexpr int NPAIRS = MT * (MT + 1) / 2;
+        // Tile (mt, nt) of B (with_k) and / or of A (with_q).
+        auto gram_tile = [&](int mt, int nt, auto with_k, auto with_q) {
+            constexpr bool WK = decltype(with_k)::value, WQ = decltype(with_q)::value;
+            f32x16 gkk = {}, gqk = {};
+            const __bf16 *ak_row = Xh + (32 * mt + l32) * XS + 8 * hg;
+            const __bf16 *aq_row = Xh + (NP + 32 * mt + l32) * XS + 8 * hg;
+            const __bf16 *bk_row = Xh + (32 * nt + l32) * XS + 8 * hg;
+#pragma unroll 2
+            for (int s = 0; s < 8; ++s) {
+                const bf16x8 bk = *reinterpret_cast<const bf16x8 *>(bk_row + 16 * s);
+                bf16x8 ak, aq;
+                if constexpr (WK) ak = *reinterpret_cast<const bf16x8 *>(ak_row + 16 * s);
+                if constexpr (WQ) aq = *reinterpret_cast<const bf16x8 *>(aq_row + 16 * s);
+                if constexpr (WK) gkk = mma(ak, bk, gkk);
+                if constexpr (WQ) gqk = mma(aq, bk, gqk);
+                if constexpr (F32IN) {
+                    const ptrdiff_t lo = Xl - Xh;
+                    const bf16x8 bkl = *reinterpret_cast<const bf16x8 *>(bk_row + lo + 16 * s);
+                    if constexpr (WK) {
+                        const bf16x8 akl = *reinterpret_cast<const bf16x8 *>(ak_row + lo + 16 * s);
+                        gkk = mma(ak, bkl, gkk);
+                        gkk = mma(akl, bk, gkk);
+                    }
+                    if constexpr (WQ) {
+                        const bf16x8 aql = *reinterpret_cast<const bf16x8 *>(aq_row + lo + 16 * s);
+                        gqk = mma(aq, bkl, gqk);
+                        gqk = mma(aql, bk, gqk);
+                    }
+                }
+            }
+            const int ci = 32 * nt + l32;
+            const float inv_mi = 1.f / gm_s[ci];
+            const int ei = ge_s[ci];
+            // The accumulator rows come in runs of four consecutive nodes, so
+            // their decays, betas and ancestor masks arrive as 16-byte LDS
+            // broadcasts; bit ci of a mask sits in word nt of the row's u64.
+#pragma unroll
+            for (int r4 = 0; r4 < 16; r4 += 4) {
+                const int t0 = 32 * mt + acc_row(r4, hg);      // rows t0 .. t0 + 3
+                const f32x4 g4 = *reinterpret_cast<const f32x4 *>(gm_s + t0);
+                const int4 e4 = *reinterpret_cast<const int4 *>(ge_s + t0);
+                const uint4 m01 = *reinterpret_cast<const uint4 *>(anc_s + t0);
+                const uint4 m23 = *reinterpret_cast<const uint4 *>(anc_s + t0 + 2);
+                const uint32_t w[4] = {nt ? m01.y : m01.x, nt ? m01.w : m01.z,
+                                       nt ? m23.y : m23.x, nt ? m23.w : m23.z};
+                f32x4 b4 = {};
+                if constexpr (WK) b4 = *reinterpret_cast<const f32x4 *>(be_s + t0);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int r = r4 + e, t = t0 + e;
+                    const bool strict = (w[e] >> l32) & 1u;
+                    const int et = e == 0 ? e4.x : e == 1 ? e4.y : e == 2 ? e4.z : e4.w;
+                    const float ratio = strict ? DecayX::ratio(g4[e], et, inv_mi, ei) : (ci == t ? 1.f : 0.f);
+                    if constexpr (WK) Bm[t * MS + ci] = strict ? b4[e] * ratio * gkk[r] : 0.f;
+                    if constexpr (WQ) Am[t * MS + ci] = ratio * gqk[r];
+                }
+            }
+        };
+        using Yes = std::true_type;
+        using No = std::false_type;
+        if constexpr (EARLY_P) {
+            // One tile: its two products on waves 0 and 1; waves 2 and 3 run
+            // their share of P meanwhile (wave 3 builds T after the barrier,
+            // while waves 0 and 1 run theirs).
+            if (wave == 0)
+                gram_tile(0, 0, Yes{}, No{});
+            else if (wave == 1)
+                gram_tile(0, 0, No{}, Yes{});
+            else
+                run_p();
+        } else if (wave < NPAIRS) {
+            gram_tile(wave == 0 ? 0 : 1, wave == 2 ? 1 : 0, Yes{}, Yes{});
+        } else if (MT == 2 && wave == 3) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int t = acc_row(r, hg);
+                Bm[t * MS + 32 + l32] = 0.f;
+                Am[t * MS + 32 + l32] = 0.f;
+            }
+        }
+
+        __syncthreads();
+        // (fused commit, long path: see rank_block)
         if (FUSE && clen > CL) {                        // long path: pass by pass, once S_old is in
             for (int l0 = 0; l0 < clen; l0 += CL) {      // uniform loop
                 if (l0 > 0) {
@@ -724,8 +813,6 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 }
             }
         }
-        const rsrc_t rn = make_rsrc(FUSE ? static_cast<char *>(cm.S_new) + (size_t)u * D * D * SB : nullptr,
-                                    FUSE ? D * D * SB : 0);
         const bool shallow = *shallow_s != 0;
         // ---- phase 3a: rows of T = (I + B)^{-1}, on wave 3 while the others start on P
         // (T (I + B))[t, j] = 0 for j != t gives, walking t's ancestors j from
@@ -833,68 +920,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             }
         }
 
-        // ---- phase 3: P = [K; Q] S0^T for this wave's 32 columns ----------
-        // The A operands (rows of [K; Q] in LDS) are double-buffered one
-        // K-step ahead; the scheduling barriers keep the compiler from
-        // hoisting every step's operands at once.
-        f32x16 accp[2 * MT];
-#pragma unroll
-        for (int m = 0; m < 2 * MT; ++m) accp[m] = f32x16{};
-        {
-            // (one buffer in the fused variant, whose update block needs the registers)
-            constexpr int NBUF = FUSE ? 1 : 2;
-            bf16x8 afr[NBUF][2 * MT], alo[NBUF][2 * MT];
-            auto load_a = [&](int buf, int s) {
-#pragma unroll
-                for (int m = 0; m < 2 * MT; ++m) {
-                    const __bf16 *arow = Xh + (32 * m + l32) * XS + 16 * s + 8 * hg;
-                    afr[buf][m] = *reinterpret_cast<const bf16x8 *>(arow);
-                    if constexpr (F32IN) alo[buf][m] = *reinterpret_cast<const bf16x8 *>(arow + (Xl - Xh));
-                }
-            };
-            if (NBUF == 2) load_a(0, 0);
-            f32x16 dcur = {};
-#pragma unroll
-            for (int s = 0; s < 8; ++s) {
-                if (NBUF == 1)
-                    load_a(0, s);
-                else if (s < 7)
-                    load_a((s + 1) & 1, s + 1);
-                if constexpr (FUSE) {                    // S0 pieces of step s: commit update
-                    if (upd_in_p) {
-                        if ((s & 1) == 0) dcur = rank_block(s >> 1, f32x16{});
-#pragma unroll
-                        for (int h = 0; h < 2; ++h) {
-                            f32x4 x = rd.sget(s, h);
-#pragma unroll
-                            for (int i = 0; i < 4; ++i) x[i] = fmaf(ga, x[i], dcur[8 * (s & 1) + 4 * h + i]);
-                            rd.sset(s, h, x);                   // a bf16 state is rounded here, then used
-                        }
-                    }
-                }
-                bf16x8 bh, bl;
-                if constexpr (SBF) {                     // a bf16 state is exact on the matrix cores
-                    bh = __builtin_bit_cast(bf16x8, make_uint4(rd.s0[s][0].x, rd.s0[s][0].y, rd.s0[s][1].x,
-                                                               rd.s0[s][1].y));
-                } else {
-                    float sv[8];
-                    *reinterpret_cast<f32x4 *>(sv) = rd.s0[s][0];
-                    *reinterpret_cast<f32x4 *>(sv + 4) = rd.s0[s][1];
-                    split8(sv, bh, bl);
-                }
-#pragma unroll
-                for (int m = 0; m < 2 * MT; ++m) {
-                    accp[m] = mma(afr[s % NBUF][m], bh, accp[m]);
-                    if constexpr (!SBF) accp[m] = mma(afr[s % NBUF][m], bl, accp[m]);
-                    if constexpr (F32IN) accp[m] = mma(alo[s % NBUF][m], bh, accp[m]);
-                }
-                // S_new leaves line by line once the steps that hold a line are done.
-                if constexpr (FUSE) {
-                    if (s % Reads::LINE_STEPS == Reads::LINE_STEPS - 1) rd.store_state_line(rn, s / Reads::LINE_STEPS, wave, lane);
-                }
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        }
+        // ---- phase 3: P (see run_p), for the waves that have not run it yet
+        if (!EARLY_P || wave < 2) run_p();
         __builtin_amdgcn_s_setprio(0);                  // (wave 3 after a deep solve)
         __syncthreads();
 
