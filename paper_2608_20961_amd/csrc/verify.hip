@@ -758,7 +758,12 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                     const int r = r4 + e, t = t0 + e;
                     const bool strict = (w[e] >> l32) & 1u;
                     const int et = e == 0 ? e4.x : e == 1 ? e4.y : e == 2 ? e4.z : e4.w;
-                    const float ratio = strict ? DecayX::ratio(g4[e], et, inv_mi, ei) : (ci == t ? 1.f : 0.f);
+                    // (the ratio is formed for every entry and then selected:
+                    // left to the compiler, the selection became a branch per
+                    // entry that waited on its own LDS read)
+                    float rs = DecayX::ratio(g4[e], et, inv_mi, ei);
+                    asm volatile("" : "+v"(rs));
+                    const float ratio = strict ? rs : (ci == t ? 1.f : 0.f);
                     if constexpr (WK) Bm[t * MS + ci] = strict ? b4[e] * ratio * gkk[r] : 0.f;
                     if constexpr (WQ) Am[t * MS + ci] = ratio * gqk[r];
                 }
@@ -824,7 +829,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // ancestors into registers first.
         if (shallow && wave == 3 && lane < NP) {
             const int t = lane;
-            const uint64_t anc = t < N ? anc_s[t] : 0ull;
+            const uint64_t anc = anc_s[t];              // (zero past the last node)
             int a[FAST];                                 // a[0] = parent(t), a[1] = its parent, ...
             uint64_t rem = anc;
 #pragma unroll
@@ -832,13 +837,16 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 a[kk] = rem ? 63 - __builtin_clzll(rem) : t;
                 rem &= ~(1ull << (a[kk] & 63));
             }
-            const int m = __popcll(anc);
+            // Past the m ancestors, a[kk] = t: those reads fetch B[t, t] and
+            // B[a[l], t] (a[l] < t), which are zero, so every read is made
+            // unconditionally (conditional reads became a branch and a wait
+            // each) and the x past m come out zero.
             float bt[FAST], bb[FAST][FAST], x[FAST];
 #pragma unroll
             for (int kk = 0; kk < FAST; ++kk) {
-                bt[kk] = kk < m ? Bm[t * MS + a[kk]] : 0.f;
+                bt[kk] = Bm[t * MS + a[kk]];
 #pragma unroll
-                for (int l = 0; l < kk; ++l) bb[l][kk] = kk < m ? Bm[a[l] * MS + a[kk]] : 0.f;
+                for (int l = 0; l < kk; ++l) bb[l][kk] = Bm[a[l] * MS + a[kk]];
             }
 #pragma unroll
             for (int kk = 0; kk < FAST; ++kk) {
@@ -847,11 +855,11 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 for (int l = 0; l < kk; ++l) acc += x[l] * bb[l][kk];
                 x[kk] = -acc;
             }
+            // (every read of B above precedes these stores)
             float *Tt = Bm + t * MS;
-            if (t < N) Tt[t] = 1.f;
 #pragma unroll
-            for (int kk = 0; kk < FAST; ++kk)
-                if (kk < m) Tt[a[kk]] = x[kk];
+            for (int kk = 0; kk < FAST; ++kk) Tt[a[kk]] = x[kk];   // past m: a zero on the diagonal
+            if (t < N) Tt[t] = 1.f;
         }
         // Deeper trees: the same recurrence as a dense column sweep.  Lane t
         // keeps r[j] = sum over the finished columns i of T[t, i] B[i, j]; at
@@ -1072,7 +1080,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                             const int r = r4 + e, t = t0 + e;
                             const bool a = (anc_all[(base + t) * MASK_WORDS + j] >> i) & 1ull;
                             const int et = e == 0 ? e4.x : e == 1 ? e4.y : e == 2 ? e4.z : e4.w;
-                            const float ratio = DecayX::ratio(m4[e], et, inv_mi, ei);
+                            float ratio = DecayX::ratio(m4[e], et, inv_mi, ei);
+                            asm volatile("" : "+v"(ratio));      // (selected below, not branched on)
                             Ck[t * MS + i] = a ? -b4[e] * ratio * gkk[r] : 0.f;
                             Cq[t * MS + i] = a ? gqk[r] * ratio : 0.f;
                         }
