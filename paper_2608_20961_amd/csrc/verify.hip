@@ -645,7 +645,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         f32x16 accp[2 * MT];
         auto run_p = [&]() {
 #pragma unroll
-        for (int m = 0; m < 2 * MT; ++m) accp[m] = f32x16{};
+            for (int m = 0; m < 2 * MT; ++m) accp[m] = f32x16{};
             // (one buffer in the fused variant, whose update block needs the registers)
             constexpr int NBUF = FUSE ? 1 : 2;
             bf16x8 afr[NBUF][2 * MT], alo[NBUF][2 * MT];
@@ -658,6 +658,19 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 }
             };
             if (NBUF == 2) load_a(0, 0);
+            // An fp32 state's operand for step s + 1 is split into hi / lo
+            // bf16 during step s, so that the conversion runs beside the
+            // matrix instructions instead of ahead of them (unfused: the
+            // fused update changes the state right before its step).
+            constexpr bool SPLIT_AHEAD = !FUSE && !SBF;
+            auto split_state = [](const auto &st, int s, bf16x8 &h, bf16x8 &l) {   // (instantiated for an fp32 state only)
+                float sv[8];
+                *reinterpret_cast<f32x4 *>(sv) = st.s0[s][0];
+                *reinterpret_cast<f32x4 *>(sv + 4) = st.s0[s][1];
+                split8(sv, h, l);
+            };
+            bf16x8 nbh, nbl;
+            if constexpr (SPLIT_AHEAD) split_state(rd, 0, nbh, nbl);
             f32x16 dcur = {};
 #pragma unroll
             for (int s = 0; s < 8; ++s) {
@@ -681,11 +694,12 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 if constexpr (SBF) {                     // a bf16 state is exact on the matrix cores
                     bh = __builtin_bit_cast(bf16x8, make_uint4(rd.s0[s][0].x, rd.s0[s][0].y, rd.s0[s][1].x,
                                                                rd.s0[s][1].y));
+                } else if constexpr (SPLIT_AHEAD) {
+                    bh = nbh;
+                    bl = nbl;
+                    if (s < 7) split_state(rd, s + 1, nbh, nbl);
                 } else {
-                    float sv[8];
-                    *reinterpret_cast<f32x4 *>(sv) = rd.s0[s][0];
-                    *reinterpret_cast<f32x4 *>(sv + 4) = rd.s0[s][1];
-                    split8(sv, bh, bl);
+                    split_state(rd, s, bh, bl);
                 }
 #pragma unroll
                 for (int m = 0; m < 2 * MT; ++m) {
