@@ -362,6 +362,51 @@ def snapshot_comparison(torch, tw, acc, w, x, d, o, ms_treewy_step, steps):
     return out
 
 
+def launch_context(torch, tw, acc, w, d, flush, steps):
+    """For a workload small enough to be flushed between launches, what the
+    single flushed launch is measured against: a plain device copy that moves
+    the verify's algorithmic bytes (half read, half written) under the same
+    flush and events, and the verify run back to back over R distinct input
+    sets, as consecutive layers would be, with R x the bytes >= 1 GiB so that
+    no set is still in the last-level cache when its turn comes (per-launch
+    time = the interval / R)."""
+    vb = acc.verify_bytes(w)
+    half = torch.empty(vb // 8, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(half)
+    _, (ms_copy,) = time_steps(torch, [lambda: dst.copy_(half)], steps, 3, flush)
+    del half, dst
+    R = int(min(32, max(2, -(-(1 << 30) // vb))))
+    sets = []
+    for _ in range(R):
+        c = {n: d[n].clone() for n in ("S0", "q", "k", "v", "alpha", "beta", "parent")}
+        c["U"] = torch.empty((w.B, w.H, w.N, w.d_v), dtype=torch.float32, device="cuda")
+        c["o"] = torch.empty((w.B, w.H, w.N, w.d_v), dtype=d["q"].dtype, device="cuda")
+        sets.append(c)
+
+    def layers():
+        for c in sets:
+            tw.treewy_verify(c["S0"], c["q"], c["k"], c["v"], c["alpha"], c["beta"], c["parent"], o=c["o"], U=c["U"])
+    # Captured in one HIP graph (as a serving loop would run a decode step),
+    # so that the host's per-call cost does not pace the launches.
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        layers()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        layers()
+    _, (ms_r,) = time_steps(torch, [graph.replay], max(3, steps // 4), 1)
+    del graph, sets
+    torch.cuda.empty_cache()
+    return {"copy_same_bytes": dict(roofline(vb, ms_copy, None), what="torch copy_ of verify_bytes / 2 each way, "
+                                                                      "flushed and timed like the verify"),
+            "verify_back_to_back": dict(roofline(vb, ms_r / R, None), input_sets=R,
+                                        what="R launches over R distinct input sets captured in one HIP graph; "
+                                             "one replay's interval / R")}
+
+
 def measure_workload(torch, tw, wl, acc, w, x, d, args, src_hash, snapshot):
     """One workload's block on the GPU: verify + commit steps (the headline's
     step on this workload), the fused call and optionally the snapshot
@@ -404,6 +449,12 @@ def measure_workload(torch, tw, wl, acc, w, x, d, args, src_hash, snapshot):
     }
     log("%s: verify %.4f, commit %.4f, fused %.4f ms" % (w.name, ms_v, ms_c, ms_f))
     del S_f, o_f, U_f
+    if flush is not None:
+        ctx = launch_context(torch, tw, acc, w, d, flush, args.steps)
+        ctx["verify_over_copy_time"] = round(ms_v / ctx["copy_same_bytes"]["avg_launch_ms"], 3)
+        block["verify"]["launch_context"] = ctx
+        log("%s: copy of the same bytes %.4f ms; verify back to back %.4f ms" % (
+            w.name, ctx["copy_same_bytes"]["avg_launch_ms"], ctx["verify_back_to_back"]["avg_launch_ms"]))
     if snapshot:
         block["snapshot_comparison"] = snapshot_comparison(torch, tw, acc, w, x, d, o, ms_step,
                                                            max(3, args.steps // 10))
