@@ -1199,12 +1199,12 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         const rsrc_t ru = make_rsrc(PRE ? nullptr : U + (unode0 + base) * D, PRE ? 0 : N * D * 4);
         const rsrc_t ro = make_rsrc(o + node0 * D, N * D * (int)sizeof(In));
         // U leaves while A U runs (rows of padding nodes fall past the end of
-        // the descriptor and are dropped).  At 64 nodes in one pass, straight
-        // from the accumulators: each store instruction writes the lane
-        // group's 32 columns, one whole 128-byte line, of two rows.  Otherwise
+        // the descriptor and are dropped).  In one pass, straight from the
+        // accumulators: each store instruction writes the lane group's 32
+        // columns, one whole 128-byte line, of two rows.  In the chunked modes
         // (where those registers are not to spare) through LDS as whole rows,
         // 16 bytes per lane.
-        constexpr bool U_DIRECT = MODE == ONE_PASS && NP == 64;
+        constexpr bool U_DIRECT = MODE == ONE_PASS;
         if constexpr (U_DIRECT) {
 #pragma unroll
             for (int m = 0; m < MT; ++m)
@@ -1243,7 +1243,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             }
             __builtin_amdgcn_sched_barrier(0);
         }
-        // At 64 nodes and in the chain prefill, bf16 o straight from the
+        // In one pass and in the chain prefill, bf16 o straight from the
         // accumulators as well.  A store instruction writes half a line (32
         // bf16) of two rows; the default policy lets L2 merge the halves from
         // neighbouring waves (rows of padding nodes fall past the descriptor).
