@@ -206,16 +206,30 @@ class TimingEvent:
             self._hip.hipEventDestroy(self.ev)
 
 
-def time_steps(torch, launches, steps, warmup, flush=None, stats=None):
+SETTLE_MS = 40.0
+
+
+def time_steps(torch, launches, steps, warmup, flush=None, stats=None, settle_ms=0.0):
     """Run `launches` (a list of callables, one step) W + K times; return the
     average step time and the average time of each launch (HIP timing
     events on the stream the kernels run on).  With `flush`, it runs between
     steps (outside every launch's events) and the step time is the sum of the
     launch times.  With `stats` (a list), the p10 / p50 / p90 of each
-    launch's times are appended to it."""
-    for _ in range(warmup):
+    launch's times are appended to it.  With `settle_ms`, warm-up steps go on
+    past W until that much wall time has passed: the GPU's clocks take tens
+    of milliseconds of sustained work to reach their level under load (a
+    fused launch timed after 5 warm-up launches ran 388 us against 335 us
+    once settled), and the headline aside every section is timed settled."""
+    t0 = time.perf_counter()
+    n = 0
+    while n < warmup or (time.perf_counter() - t0) * 1e3 < settle_ms:
+        if flush is not None and n >= warmup:
+            flush()
         for f in launches:
             f()
+        n += 1
+        if settle_ms > 0 and n % 8 == 0:
+            torch.cuda.synchronize()                # (wall time then follows the GPU)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     ev = [[TimingEvent() for _ in range(len(launches) + 1)] for _ in range(steps)]
@@ -373,7 +387,7 @@ def launch_context(torch, tw, acc, w, d, flush, steps):
     vb = acc.verify_bytes(w)
     half = torch.empty(vb // 8, dtype=torch.float32, device="cuda").fill_(1.0)
     dst = torch.empty_like(half)
-    _, (ms_copy,) = time_steps(torch, [lambda: dst.copy_(half)], steps, 3, flush)
+    _, (ms_copy,) = time_steps(torch, [lambda: dst.copy_(half)], steps, 3, flush, settle_ms=SETTLE_MS)
     del half, dst
     R = int(min(32, max(2, -(-(1 << 30) // vb))))
     sets = []
@@ -397,7 +411,7 @@ def launch_context(torch, tw, acc, w, d, flush, steps):
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
         layers()
-    _, (ms_r,) = time_steps(torch, [graph.replay], max(3, steps // 4), 1)
+    _, (ms_r,) = time_steps(torch, [graph.replay], max(3, steps // 4), 1, settle_ms=SETTLE_MS)
     del graph, sets
     torch.cuda.empty_cache()
     return {"copy_same_bytes": dict(roofline(vb, ms_copy, None), what="torch copy_ of verify_bytes / 2 each way, "
@@ -426,7 +440,8 @@ def measure_workload(torch, tw, wl, acc, w, x, d, args, src_hash, snapshot):
 
     flush = make_flush(torch, acc, w, x["path_len"])
     dist = []
-    ms_step, (ms_v, ms_c) = time_steps(torch, [verify, commit], args.steps, args.warmup, flush, dist)
+    ms_step, (ms_v, ms_c) = time_steps(torch, [verify, commit], args.steps, args.warmup, flush, dist,
+                                       settle_ms=SETTLE_MS)
     S_f, o_f, U_f = torch.empty_like(d["S0"]), torch.empty_like(o), torch.empty_like(U)
 
     def fused():
@@ -434,7 +449,7 @@ def measure_workload(torch, tw, wl, acc, w, x, d, args, src_hash, snapshot):
                                 d["alpha"], d["beta"], d["parent"], parent_prev=d["parent"], S_new=S_f, o=o_f,
                                 U=U_f)
 
-    _, (ms_f,) = time_steps(torch, [fused], args.steps, args.warmup, flush)
+    _, (ms_f,) = time_steps(torch, [fused], args.steps, args.warmup, flush, settle_ms=SETTLE_MS)
     nodes = w.B * w.N
     block = {
         "workload": w.describe(), "units": w.units, "ms_per_step": round(ms_step, 5),
@@ -558,7 +573,7 @@ def main():
                                 d["alpha"], d["beta"], d["parent"], parent_prev=d["parent"], S_new=S_fused, o=o_f,
                                 U=U_f)
 
-    _, (ms_fused,) = time_steps(torch, [fused], args.steps, args.warmup, flush)
+    _, (ms_fused,) = time_steps(torch, [fused], args.steps, args.warmup, flush, settle_ms=SETTLE_MS)
     log("fused commit+verify: %.4f ms/launch" % ms_fused)
     fb = acc.commit_verify_bytes(w, x["path_len"])
     result["fused_commit_verify"] = dict(
@@ -587,8 +602,9 @@ def main():
                                     S_new=S_new_b, o=o_f2, U=U_f2)
 
         o_f2, U_f2 = torch.empty_like(o), torch.empty_like(U)
-        ms_step_b, (ms_vb, ms_cb) = time_steps(torch, [verify_b, commit_b], args.steps, args.warmup, flush)
-        _, (ms_fb,) = time_steps(torch, [fused_b], args.steps, args.warmup, flush)
+        ms_step_b, (ms_vb, ms_cb) = time_steps(torch, [verify_b, commit_b], args.steps, args.warmup, flush,
+                                               settle_ms=SETTLE_MS)
+        _, (ms_fb,) = time_steps(torch, [fused_b], args.steps, args.warmup, flush, settle_ms=SETTLE_MS)
         log("bf16 state: verify %.4f, commit %.4f, fused %.4f ms" % (ms_vb, ms_cb, ms_fb))
         result["bf16_state"] = {
             "ms_per_step": round(ms_step_b, 5), "nodes_per_s": round(nodes / (ms_step_b * 1e-3), 1),
@@ -607,7 +623,7 @@ def main():
         def prefill():
             tw.treewy_chain_prefill(d["S0"], qp, kp, vp, ap, bp, S_T=S_p, o=o_p)
 
-        _, (ms_pf,) = time_steps(torch, [prefill], max(3, args.steps // 10), 1)
+        _, (ms_pf,) = time_steps(torch, [prefill], max(3, args.steps // 10), 1, settle_ms=SETTLE_MS)
         pb = acc.prefill_bytes(w, Tp)
         result["chain_prefill"] = dict(roofline(pb, ms_pf, load_traffic("chain_prefill", w.name, src_hash)), tokens=Tp,
                                        tokens_per_s=round(w.B * Tp / (ms_pf * 1e-3), 1))
@@ -627,7 +643,7 @@ def main():
             tw.treewy_commit(S0_commit, U_b, bk, ba, bpath, bplen, parent=bpar, S_new=S_nb)
 
         ms_bstep, (ms_bv, ms_bc) = time_steps(torch, [verify_big, commit_big], max(5, args.steps // 2),
-                                              max(2, args.warmup // 2))
+                                              max(2, args.warmup // 2), settle_ms=SETTLE_MS)
         nb = wb.B * wb.N
         result["tree128"] = {
             "workload": wb.describe(),
@@ -650,14 +666,14 @@ def main():
         tw.treewy_accept_greedy(d["parent"], t_d, t_t, t_r, w.max_depth, path=acc_path, path_len=acc_len,
                                 bonus=acc_bonus)
 
-    _, (ms_acc,) = time_steps(torch, [accept], args.steps, args.warmup)
+    _, (ms_acc,) = time_steps(torch, [accept], args.steps, args.warmup, settle_ms=SETTLE_MS)
     result["accept_greedy"] = {"avg_launch_ms": round(ms_acc, 5), "sequences": w.B, "nodes": w.N,
                                "mean_accepted": round(float(acc_len.float().mean()), 3)}
     # What a plain device-to-device copy reaches on this GPU (read + write
     # bytes): the practical ceiling next to the 8 TB/s vendor peak.
     src = torch.ones(1 << 28, device="cuda")
     dst = torch.empty_like(src)
-    _, (ms_copy,) = time_steps(torch, [lambda: dst.copy_(src)], 10, 3)
+    _, (ms_copy,) = time_steps(torch, [lambda: dst.copy_(src)], 10, 3, settle_ms=SETTLE_MS)
     result["hbm_copy_achievable"] = {"GB_per_s": round(2 * 4 * (1 << 28) / (ms_copy * 1e-3) / 1e9, 1),
                                      "bytes_each_way": 4 * (1 << 28), "avg_launch_ms": round(ms_copy, 5)}
     del src, dst
