@@ -207,9 +207,12 @@ class TimingEvent:
 
 
 SETTLE_MS = 40.0
+# Every timed section in launch order: its tag, its warm-up and timed steps
+# (so that a kernel trace of this command can be split into sections).
+LAUNCH_LOG = []
 
 
-def time_steps(torch, launches, steps, warmup, flush=None, stats=None, settle_ms=0.0):
+def time_steps(torch, launches, steps, warmup, flush=None, stats=None, settle_ms=0.0, tag=None, per_step=None):
     """Run `launches` (a list of callables, one step) W + K times; return the
     average step time and the average time of each launch (HIP timing
     events on the stream the kernels run on).  With `flush`, it runs between
@@ -219,7 +222,9 @@ def time_steps(torch, launches, steps, warmup, flush=None, stats=None, settle_ms
     past W until that much wall time has passed: the GPU's clocks take tens
     of milliseconds of sustained work to reach their level under load (a
     fused launch timed after 5 warm-up launches ran 388 us against 335 us
-    once settled), and the headline aside every section is timed settled."""
+    once settled), and the headline aside every section is timed settled.
+    `tag` names the section in LAUNCH_LOG; `per_step` lists how many kernels
+    each callable launches when that is not one."""
     t0 = time.perf_counter()
     n = 0
     while n < warmup or (time.perf_counter() - t0) * 1e3 < settle_ms:
@@ -231,6 +236,8 @@ def time_steps(torch, launches, steps, warmup, flush=None, stats=None, settle_ms
         if settle_ms > 0 and n % 8 == 0:
             torch.cuda.synchronize()                # (wall time then follows the GPU)
     torch.cuda.synchronize()
+    LAUNCH_LOG.append({"tag": tag, "warmup_steps": n, "timed_steps": steps,
+                       "kernels_per_step": per_step if per_step is not None else [1] * len(launches)})
     stream = torch.cuda.current_stream()
     ev = [[TimingEvent() for _ in range(len(launches) + 1)] for _ in range(steps)]
     t0 = TimingEvent()
@@ -351,7 +358,7 @@ def snapshot_comparison(torch, tw, acc, w, x, d, o, ms_treewy_step, steps):
     def scommit():
         tw.treewy_snapshot_commit(d["S0"], snaps, acc_node, S_new=S_new)
 
-    ms_s, (ms_sv, ms_sc) = time_steps(torch, [sverify, scommit], steps, 1)
+    ms_s, (ms_sv, ms_sc) = time_steps(torch, [sverify, scommit], steps, 1, tag=w.name + ".snapshot")
     sb = acc.snapshot_verify_bytes(w)
     reload = acc.snapshot_reload_bytes(w, x["parent"])
     spec = acc.speculative_state_bytes(w)
@@ -387,7 +394,8 @@ def launch_context(torch, tw, acc, w, d, flush, steps):
     vb = acc.verify_bytes(w)
     half = torch.empty(vb // 8, dtype=torch.float32, device="cuda").fill_(1.0)
     dst = torch.empty_like(half)
-    _, (ms_copy,) = time_steps(torch, [lambda: dst.copy_(half)], steps, 3, flush, settle_ms=SETTLE_MS)
+    _, (ms_copy,) = time_steps(torch, [lambda: dst.copy_(half)], steps, 3, flush, settle_ms=SETTLE_MS,
+                               tag=w.name + ".copy")
     del half, dst
     R = int(min(32, max(2, -(-(1 << 30) // vb))))
     sets = []
@@ -408,10 +416,12 @@ def launch_context(torch, tw, acc, w, d, flush, steps):
         layers()
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
+    LAUNCH_LOG.append({"tag": w.name + ".graph_warm", "warmup_steps": 1, "timed_steps": 0, "kernels_per_step": [R]})
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
         layers()
-    _, (ms_r,) = time_steps(torch, [graph.replay], max(3, steps // 4), 1, settle_ms=SETTLE_MS)
+    _, (ms_r,) = time_steps(torch, [graph.replay], max(3, steps // 4), 1, settle_ms=SETTLE_MS,
+                            tag=w.name + ".graph", per_step=[R])
     del graph, sets
     torch.cuda.empty_cache()
     return {"copy_same_bytes": dict(roofline(vb, ms_copy, None), what="torch copy_ of verify_bytes / 2 each way, "
@@ -441,7 +451,7 @@ def measure_workload(torch, tw, wl, acc, w, x, d, args, src_hash, snapshot):
     flush = make_flush(torch, acc, w, x["path_len"])
     dist = []
     ms_step, (ms_v, ms_c) = time_steps(torch, [verify, commit], args.steps, args.warmup, flush, dist,
-                                       settle_ms=SETTLE_MS)
+                                       settle_ms=SETTLE_MS, tag=w.name + ".verify_commit")
     S_f, o_f, U_f = torch.empty_like(d["S0"]), torch.empty_like(o), torch.empty_like(U)
 
     def fused():
@@ -449,7 +459,8 @@ def measure_workload(torch, tw, wl, acc, w, x, d, args, src_hash, snapshot):
                                 d["alpha"], d["beta"], d["parent"], parent_prev=d["parent"], S_new=S_f, o=o_f,
                                 U=U_f)
 
-    _, (ms_f,) = time_steps(torch, [fused], args.steps, args.warmup, flush, settle_ms=SETTLE_MS)
+    _, (ms_f,) = time_steps(torch, [fused], args.steps, args.warmup, flush, settle_ms=SETTLE_MS,
+                            tag=w.name + ".fused")
     nodes = w.B * w.N
     block = {
         "workload": w.describe(), "units": w.units, "ms_per_step": round(ms_step, 5),
@@ -559,6 +570,7 @@ def main():
     flush = make_flush(torch, acc, w, x["path_len"])
     verify()                                       # U for the fused call's previous round
     torch.cuda.synchronize()
+    LAUNCH_LOG.append({"tag": "head.verify_for_U", "warmup_steps": 1, "timed_steps": 0, "kernels_per_step": [1]})
     nodes = w.B * w.N
     result = {}
     # Fused: the previous round's commit inside this round's verify
@@ -573,7 +585,8 @@ def main():
                                 d["alpha"], d["beta"], d["parent"], parent_prev=d["parent"], S_new=S_fused, o=o_f,
                                 U=U_f)
 
-    _, (ms_fused,) = time_steps(torch, [fused], args.steps, args.warmup, flush, settle_ms=SETTLE_MS)
+    _, (ms_fused,) = time_steps(torch, [fused], args.steps, args.warmup, flush, settle_ms=SETTLE_MS,
+                                tag="head.fused")
     log("fused commit+verify: %.4f ms/launch" % ms_fused)
     fb = acc.commit_verify_bytes(w, x["path_len"])
     result["fused_commit_verify"] = dict(
@@ -603,8 +616,9 @@ def main():
 
         o_f2, U_f2 = torch.empty_like(o), torch.empty_like(U)
         ms_step_b, (ms_vb, ms_cb) = time_steps(torch, [verify_b, commit_b], args.steps, args.warmup, flush,
-                                               settle_ms=SETTLE_MS)
-        _, (ms_fb,) = time_steps(torch, [fused_b], args.steps, args.warmup, flush, settle_ms=SETTLE_MS)
+                                               settle_ms=SETTLE_MS, tag="head.bf16_verify_commit")
+        _, (ms_fb,) = time_steps(torch, [fused_b], args.steps, args.warmup, flush, settle_ms=SETTLE_MS,
+                                 tag="head.bf16_fused")
         log("bf16 state: verify %.4f, commit %.4f, fused %.4f ms" % (ms_vb, ms_cb, ms_fb))
         result["bf16_state"] = {
             "ms_per_step": round(ms_step_b, 5), "nodes_per_s": round(nodes / (ms_step_b * 1e-3), 1),
@@ -623,7 +637,8 @@ def main():
         def prefill():
             tw.treewy_chain_prefill(d["S0"], qp, kp, vp, ap, bp, S_T=S_p, o=o_p)
 
-        _, (ms_pf,) = time_steps(torch, [prefill], max(3, args.steps // 10), 1, settle_ms=SETTLE_MS)
+        _, (ms_pf,) = time_steps(torch, [prefill], max(3, args.steps // 10), 1, settle_ms=SETTLE_MS,
+                                 tag="head.prefill")
         pb = acc.prefill_bytes(w, Tp)
         result["chain_prefill"] = dict(roofline(pb, ms_pf, load_traffic("chain_prefill", w.name, src_hash)), tokens=Tp,
                                        tokens_per_s=round(w.B * Tp / (ms_pf * 1e-3), 1))
@@ -643,7 +658,7 @@ def main():
             tw.treewy_commit(S0_commit, U_b, bk, ba, bpath, bplen, parent=bpar, S_new=S_nb)
 
         ms_bstep, (ms_bv, ms_bc) = time_steps(torch, [verify_big, commit_big], max(5, args.steps // 2),
-                                              max(2, args.warmup // 2), settle_ms=SETTLE_MS)
+                                              max(2, args.warmup // 2), settle_ms=SETTLE_MS, tag="head.tree128")
         nb = wb.B * wb.N
         result["tree128"] = {
             "workload": wb.describe(),
@@ -666,14 +681,14 @@ def main():
         tw.treewy_accept_greedy(d["parent"], t_d, t_t, t_r, w.max_depth, path=acc_path, path_len=acc_len,
                                 bonus=acc_bonus)
 
-    _, (ms_acc,) = time_steps(torch, [accept], args.steps, args.warmup, settle_ms=SETTLE_MS)
+    _, (ms_acc,) = time_steps(torch, [accept], args.steps, args.warmup, settle_ms=SETTLE_MS, tag="head.accept")
     result["accept_greedy"] = {"avg_launch_ms": round(ms_acc, 5), "sequences": w.B, "nodes": w.N,
                                "mean_accepted": round(float(acc_len.float().mean()), 3)}
     # What a plain device-to-device copy reaches on this GPU (read + write
     # bytes): the practical ceiling next to the 8 TB/s vendor peak.
     src = torch.ones(1 << 28, device="cuda")
     dst = torch.empty_like(src)
-    _, (ms_copy,) = time_steps(torch, [lambda: dst.copy_(src)], 10, 3, settle_ms=SETTLE_MS)
+    _, (ms_copy,) = time_steps(torch, [lambda: dst.copy_(src)], 10, 3, settle_ms=SETTLE_MS, tag="head.copy")
     result["hbm_copy_achievable"] = {"GB_per_s": round(2 * 4 * (1 << 28) / (ms_copy * 1e-3) / 1e9, 1),
                                      "bytes_each_way": 4 * (1 << 28), "avg_launch_ms": round(ms_copy, 5)}
     del src, dst
@@ -686,7 +701,8 @@ def main():
 
     # ---- the headline: W warmup steps, then exactly K timed steps ------------
     dist = []
-    ms_step, (ms_verify, ms_commit) = time_steps(torch, [verify, commit], args.steps, args.warmup, flush, dist)
+    ms_step, (ms_verify, ms_commit) = time_steps(torch, [verify, commit], args.steps, args.warmup, flush, dist,
+                                                 tag="head.verify_commit")
     log("timed %d steps: %.4f ms/step (verify %.4f, commit %.4f)" % (args.steps, ms_step, ms_verify, ms_commit))
     vb = acc.verify_bytes(w)
     cb = acc.commit_bytes(w, x["path_len"])
@@ -730,6 +746,7 @@ def main():
             block["cpu_baseline"] = cpu_baseline(wo, wl, xo, args.seed, args.config_cpu_seconds, max_units=2048)
         log("cpu baseline (oracle) ...")
         result["cpu_baseline"] = cpu_baseline(w, wl, x, args.seed, args.cpu_seconds)
+    result["launch_log"] = LAUNCH_LOG
     print(json.dumps(result), flush=True)
 
 
