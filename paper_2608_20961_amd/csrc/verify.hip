@@ -636,11 +636,12 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         const bool upd_in_p = FUSE && clen > 0 && clen <= CL;
         const rsrc_t rn = make_rsrc(FUSE ? static_cast<char *>(cm.S_new) + (size_t)u * D * D * SB : nullptr,
                                     FUSE ? D * D * SB : 0);
-        // ---- P = [K; Q] S0^T for this wave's 32 columns (phase 3) -----------
-        // The A operands (rows of [K; Q] in LDS) are double-buffered one
-        // K-step ahead; the scheduling barriers keep the compiler from
-        // hoisting every step's operands at once.
-        // With 32 rows, waves 2 and 3 have no gram work and run P during the gram.
+        // ---- P = [K; Q] S0^T for this wave's 32 columns --------------------
+        // Run in phase 3, except that with 32 rows (one gram tile) waves 2 and
+        // 3 run it during the gram (EARLY_P, phase 2).  The A operands (rows
+        // of [K; Q] in LDS) are double-buffered one K-step ahead; the
+        // scheduling barriers keep the compiler from hoisting every step's
+        // operands at once.
         constexpr bool EARLY_P = NP == 32 && !FUSE;
         f32x16 accp[2 * MT];
         auto run_p = [&]() {
