@@ -252,14 +252,14 @@ struct UnitReads {
     }
 };
 
-// One column of the dense sweep that builds row t of a 32-row block of
-// T = (I + B)^{-1} (see phase 3a), then the next column down.  Compile-time
+// One column of the dense sweep that builds row t of a W-row diagonal block
+// of T = (I + B)^{-1} (see phase 3a), then the next column down.  Compile-time
 // recursion keeps every index into r static (r stays in registers).  A
 // column's row read must not be hoisted far ahead (that needs a register per
 // element of B): its address passes through an empty asm that also takes the
 // previous column's pivot, so rows are fetched one column ahead.
-template <int I, int MS>
-__device__ __forceinline__ void sweep_column(float (&r)[32], const float *Bm, int t, float prev) {
+template <int I, int MS, int W>
+__device__ __forceinline__ void sweep_column(float (&r)[W], const float *Bm, int t, float prev) {
     if constexpr (I >= 0) {
         const float x = I < t ? -r[I] : 0.f;            // T[t, I] (zero on and above the diagonal)
         r[I] = x;
@@ -894,52 +894,83 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             // here: the wave goes first at instruction issue on its SIMD until
             // P is done)
             __builtin_amdgcn_s_setprio(2);
-            const int tl = lane & 31;                                // row within a diagonal block
-            const int off = NP == 64 ? 32 * (lane >> 5) : 0;
+            // Diagonal 16-row blocks first: lanes 16 q .. 16 q + 15 sweep T_q =
+            // (I + B_qq)^{-1} in 15 column steps (two distinct broadcast
+            // addresses per half-wave read; at 32 rows lanes 32-63 repeat
+            // block 0 and store nothing).
+            const int q = lane >> 4, tl = lane & 15;
+            const bool live = 16 * q < NP;
+            const int off = live ? 16 * q : 0;
             const float *Bblk = Bm + off * MS + off;
-            float r[32];
+            float r[16];
 #pragma unroll
-            for (int c = 0; c < 8; ++c) {
+            for (int c = 0; c < 4; ++c) {
                 const f32x4 bt = *reinterpret_cast<const f32x4 *>(Bblk + tl * MS + 4 * c);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) r[4 * c + e] = bt[e];
             }
-            sweep_column<31, MS>(r, Bblk, tl, 0.f);
-            if (NP == 64 || lane < 32) {
+            sweep_column<15, MS>(r, Bblk, tl, 0.f);
+            if (live) {
                 float *Tt = Bm + (off + tl) * MS + off;
 #pragma unroll
-                for (int c = 0; c < 8; ++c)
+                for (int c = 0; c < 4; ++c)
                     *reinterpret_cast<f32x4 *>(Tt + 4 * c) = f32x4{r[4 * c], r[4 * c + 1], r[4 * c + 2], r[4 * c + 3]};
                 if (off + tl < N) Tt[tl] = 1.f;
             }
+            // 32 x 32 products on the matrix cores, KS steps of 16 deep: row
+            // l32 of the left factor from Arow, column l32 of the right one
+            // from Bcol (rows MS apart).
+            auto block_product = [&](const float *Arow, const float *Bcol, auto ks) {
+                constexpr int KS = decltype(ks)::value;
+                f32x16 acc = {};
+#pragma unroll
+                for (int s2 = 0; s2 < KS; ++s2) {
+                    float a8[8], b8[8];
+                    *reinterpret_cast<f32x4 *>(a8) = *reinterpret_cast<const f32x4 *>(Arow + 16 * s2 + 8 * hg);
+                    *reinterpret_cast<f32x4 *>(a8 + 4) = *reinterpret_cast<const f32x4 *>(Arow + 16 * s2 + 8 * hg + 4);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) b8[e] = Bcol[(16 * s2 + 8 * hg + e) * MS];
+                    bf16x8 ah, alo, bh, bl;
+                    split8(a8, ah, alo);
+                    split8(b8, bh, bl);
+                    acc = mma(ah, bh, acc);
+                    acc = mma(ah, bl, acc);
+                    acc = mma(alo, bh, acc);
+                }
+                return acc;
+            };
+            using One = std::integral_constant<int, 1>;
+            using Two = std::integral_constant<int, 2>;
+            // 16 -> 32: in each 32-row diagonal block, the lower-left 16 x 16
+            // block of its inverse is -T_1 (B_10 T_0), T_0 and T_1 being its
+            // diagonal 16-blocks.  A 16-deep product of the block's rows with
+            // its first 16 columns gives B_10 T_0 in output rows 16-31,
+            // columns 0-15 (the other outputs are not used: upper entries of
+            // B are zero), parked over B_10; a second, with the block's last
+            // 16 columns, gives T_1 (B_10 T_0) there.
+#pragma unroll
+            for (int p = 0; p < NP / 32; ++p) {
+                float *blk = Bm + 32 * p * MS + 32 * p;
+                const f32x16 mm = block_product(blk + l32 * MS, blk + l32, One{});              // B_10 T_0
+                if (l32 < 16) {
+#pragma unroll
+                    for (int r2 = 8; r2 < 16; ++r2) blk[acc_row(r2, hg) * MS + l32] = mm[r2];
+                }
+                const f32x16 tt = block_product(blk + l32 * MS + 16, blk + 16 * MS + l32, One{});  // T_1 M
+                if (l32 < 16) {
+#pragma unroll
+                    for (int r2 = 8; r2 < 16; ++r2) blk[acc_row(r2, hg) * MS + l32] = -tt[r2];
+                }
+            }
             if constexpr (NP == 64) {
-                // rows of the left factor and columns of the right one, 16 deep per step
-                auto block_product = [&](const float *Arow, const float *Bcol) {
-                    f32x16 acc = {};
-#pragma unroll
-                    for (int s2 = 0; s2 < 2; ++s2) {
-                        float a8[8], b8[8];
-                        *reinterpret_cast<f32x4 *>(a8) = *reinterpret_cast<const f32x4 *>(Arow + 16 * s2 + 8 * hg);
-                        *reinterpret_cast<f32x4 *>(a8 + 4) =
-                            *reinterpret_cast<const f32x4 *>(Arow + 16 * s2 + 8 * hg + 4);
-#pragma unroll
-                        for (int e = 0; e < 8; ++e) b8[e] = Bcol[(16 * s2 + 8 * hg + e) * MS];
-                        bf16x8 ah, alo, bh, bl;
-                        split8(a8, ah, alo);
-                        split8(b8, bh, bl);
-                        acc = mma(ah, bh, acc);
-                        acc = mma(ah, bl, acc);
-                        acc = mma(alo, bh, acc);
-                    }
-                    return acc;
-                };
+                // 32 -> 64: T10 = -T11 (B10 T00), with B10 T00 parked over B10
                 float *B10 = Bm + 32 * MS;
-                const f32x16 mm = block_product(B10 + l32 * MS, Bm + l32);            // B10 T00
+                const f32x16 mm = block_product(B10 + l32 * MS, Bm + l32, Two{});            // B10 T00
 #pragma unroll
-                for (int r = 0; r < 16; ++r) B10[acc_row(r, hg) * MS + l32] = mm[r];
-                const f32x16 tt = block_product(B10 + l32 * MS + 32, B10 + l32);       // T11 M
+                for (int r2 = 0; r2 < 16; ++r2) B10[acc_row(r2, hg) * MS + l32] = mm[r2];
+                const f32x16 tt = block_product(B10 + l32 * MS + 32, B10 + l32, Two{});       // T11 M
 #pragma unroll
-                for (int r = 0; r < 16; ++r) B10[acc_row(r, hg) * MS + l32] = -tt[r];
+                for (int r2 = 0; r2 < 16; ++r2) B10[acc_row(r2, hg) * MS + l32] = -tt[r2];
             }
         }
 
