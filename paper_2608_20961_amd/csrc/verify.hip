@@ -834,7 +834,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             }
         }
         const bool shallow = *shallow_s != 0;
-        // ---- phase 3a: rows of T = (I + B)^{-1}, on wave 3 while the others start on P
+        // ---- phase 3a: rows of T = (I + B)^{-1}, on wave 3 while the others run P
         // (T (I + B))[t, j] = 0 for j != t gives, walking t's ancestors j from
         // the nearest upwards, T[t, j] = -sum over i in {t} and the ancestors
         // of t below j of T[t, i] B[i, j], with T[t, t] = 1.  Each lane
@@ -890,9 +890,9 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // so that one accumulator tile is live at a time).  LDS accesses of
         // one wave complete in order, so no barrier separates the steps.
         if (!shallow && wave == 3) {
-            // (the solve, then this wave's share of P, is the critical path
-            // here: the wave goes first at instruction issue on its SIMD until
-            // P is done)
+            // (the solve, then at 64 rows this wave's share of P, is the
+            // critical path here: the wave goes first at instruction issue on
+            // its SIMD until then)
             __builtin_amdgcn_s_setprio(2);
             // Diagonal 16-row blocks first: lanes 16 q .. 16 q + 15 sweep T_q =
             // (I + B_qq)^{-1} in 15 column steps (two distinct broadcast
