@@ -280,7 +280,7 @@ __device__ __forceinline__ void sweep_column(float (&r)[W], const float *Bm, int
 // How a unit's nodes are walked: in one pass (at most 64 nodes), as a chain
 // in chunks of 64 tokens with the state carried between chunks (chain
 // prefill), or as a tree of more than 64 nodes in chunks of 64, each chunk
-// using S0 again and coupled to the earlier chunks.
+// using S0 (read once, held in registers) and coupled to the earlier chunks.
 constexpr int ONE_PASS = 0, CHAIN_PREFILL = 1, TREE_CHUNKS = 2;
 
 // Two workgroups per CU where 256 registers per lane suffice; fp32 inputs
@@ -452,10 +452,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         PathPiece cp;
         // (one workgroup per CU only: at two, the other workgroup hides the loads)
         constexpr bool AHEAD = PRE && F32IN;             // the chain prefill fetches the next chunk early
-        // Tree chunks read S0 again for every chunk, except with a bf16 state:
-        // its 32 registers stay live from the first chunk without spills (the
-        // fp32 state's 64 do not fit beside the coupling).
-        constexpr bool RELOAD_STATE = XT && !SBF;
+        // The chunked modes read S0 with the first chunk only and keep it in
+        // registers (tree chunks use it unchanged in every chunk).
         if constexpr (FUSE) {
             rd.template issue<STREAM>(S0, q, k, v, alpha, beta, prow, u, N, node0, false, tid, lane, wave, hg, col);
             if (wave == 3) {
@@ -469,7 +467,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             rd.issue_state(S0, u, hg, col);
         } else if (!AHEAD || chunk == 0) {               // (then later chunks were fetched one chunk ahead)
             rd.template issue<XT ? CACHED : STREAM>(S0, q, k, v, alpha, beta, prow, u, N, node0,
-                                                    chunk == 0 || RELOAD_STATE, tid, lane, wave, hg, col);
+                                                    chunk == 0, tid, lane, wave, hg, col);
         }
 
         // ---- phase 1: ancestors and cumulative decay by pointer jumping ----
