@@ -158,8 +158,9 @@ treewy_status treewy_commit_verify(const void *S_old, const float *U_prev, const
  * treewy_chain_prefill - run the gated delta rule (Background, eq. 1) over a
  * chain of T tokens per unit and return every token's output and the final
  * state.  This is the chain WY form that the tree method generalises
- * (Related work and Method: DeltaNet's chain transform): in chunks of 64
- * tokens, each chunk is one chain verify (eq. 2) from the current state, and
+ * (Related work and Method: DeltaNet's chain transform): in chunks of 32
+ * tokens (64 with fp32 tokens), each chunk is one chain verify (eq. 2) from
+ * the current state, and
  * the state after its last token is rebuilt with eq. 3 and becomes the next
  * chunk's S0.  One launch on `stream`; the state stays on chip between
  * chunks, so it is read and written once per unit.

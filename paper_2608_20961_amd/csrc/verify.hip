@@ -44,12 +44,12 @@
 //
 // Variants of the same kernel (template arguments): FUSE commits the
 // previous round's accepted path into S0 on the way in (the fused call) and
-// writes it out as S_new; MODE walks a unit's nodes in 64-node chunks,
-// either as a chain whose state is carried in registers from chunk to chunk
-// and updated at the end of each (the chain prefill), or as a tree of more
-// than 64 nodes, each chunk using S0 (read again per chunk for an fp32
-// state, kept in registers for a bf16 one) and coupled to the pseudo-values
-// of its ancestors in earlier chunks before its own solve.
+// writes it out as S_new; MODE walks a unit's nodes in chunks, either as a
+// chain of NP-token chunks whose state is carried in registers from chunk to
+// chunk and updated at the end of each (the chain prefill), or as a tree of
+// more than 64 nodes in 64-node chunks, each chunk using S0 (read once and
+// kept in registers) and coupled to the pseudo-values of its ancestors in
+// earlier chunks before its own solve.
 #include "device.h"
 #include "launch.h"
 
@@ -278,7 +278,7 @@ __device__ __forceinline__ void sweep_column(float (&r)[W], const float *Bm, int
 }
 
 // How a unit's nodes are walked: in one pass (at most 64 nodes), as a chain
-// in chunks of 64 tokens with the state carried between chunks (chain
+// in chunks of NP tokens with the state carried between chunks (chain
 // prefill), or as a tree of more than 64 nodes in chunks of 64, each chunk
 // using S0 (read once, held in registers) and coupled to the earlier chunks.
 constexpr int ONE_PASS = 0, CHAIN_PREFILL = 1, TREE_CHUNKS = 2;
@@ -296,7 +296,9 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
     using In = typename std::conditional<F32IN, float, __bf16>::type;
     static_assert(!(SBF && F32IN), "a bf16 state is paired with bf16 inputs");
     constexpr bool PRE = MODE == CHAIN_PREFILL, XT = MODE == TREE_CHUNKS;
-    static_assert(!(MODE != ONE_PASS && (FUSE || NP != 64)), "chunked modes run 64-node chunks, unfused");
+    static_assert(!(MODE != ONE_PASS && FUSE) && !(XT && NP != 64), "chunked modes run unfused, tree chunks of 64 nodes");
+    // Chain prefill chunks hold NP tokens (32 or 64); tree chunks 64 nodes.
+    constexpr int CN = PRE ? NP : 64;
     using L = VerifyLds<NP, F32IN, FUSE>;
     using Reads = UnitReads<NP, F32IN, FUSE, SBF, PRE>;
     constexpr int SB = Reads::SB;
@@ -378,10 +380,10 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
     constexpr int buf = 0;                               // the fused call's path metadata buffer
     {
         const int b = u / H;
-        // Chunked modes: the unit's nodes in chunks of 64 (the chain prefill
+        // Chunked modes: the unit's nodes in chunks of CN (the chain prefill
         // keeps the state in registers from one chunk to the next).
         // Otherwise one pass.
-        const int chunks = MODE != ONE_PASS ? (N_all + 63) / 64 : 1;
+        const int chunks = MODE != ONE_PASS ? (N_all + CN - 1) / CN : 1;
         for (int chunk = 0; chunk < chunks; ++chunk) {
         // Lane indices are re-derived each pass from an opaque copy so the
         // per-lane offsets below are recomputed here instead of being hoisted
@@ -390,10 +392,10 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         int tid = opaque(threadIdx.x), lane = tid & 63;
         int l32 = lane & 31, hg = lane >> 5;
         int col = wave * 32 + l32;                       // this lane's d_v column (= row of S0)
-        const int N = MODE != ONE_PASS ? (N_all - 64 * chunk < 64 ? N_all - 64 * chunk : 64) : N_all;
+        const int N = MODE != ONE_PASS ? (N_all - CN * chunk < CN ? N_all - CN * chunk : CN) : N_all;
         const int base = XT ? 64 * chunk : 0;            // tree index of this chunk's node 0
         const int32_t *prow = parent ? parent + (size_t)b * N_all + base : nullptr;
-        const size_t node0 = (size_t)u * in_stride + 64 * chunk;   // row of node 0 in q/k/v/alpha/beta/o
+        const size_t node0 = (size_t)u * in_stride + CN * chunk;   // row of node 0 in q/k/v/alpha/beta/o
         const size_t unode0 = (size_t)u * u_stride;      // ... and in U
 
         // Fused commit, per thread: one k chunk (KCH elements of d_k) and one
@@ -450,8 +452,9 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         int clen = 0;
         float ga = 1.f;
         PathPiece cp;
-        // (one workgroup per CU only: at two, the other workgroup hides the loads)
-        constexpr bool AHEAD = PRE && F32IN;             // the chain prefill fetches the next chunk early
+        // The chain prefill fetches the next chunk early where the registers
+        // allow: fp32 tokens (one workgroup per CU) and 32-token chunks.
+        constexpr bool AHEAD = PRE && (F32IN || NP == 32);
         // The chunked modes read S0 with the first chunk only and keep it in
         // registers (tree chunks use it unchanged in every chunk).
         if constexpr (FUSE) {
@@ -591,8 +594,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // chunk's arithmetic.
         if constexpr (AHEAD) {
             if (chunk + 1 < chunks) {
-                const int N1 = N_all - 64 * (chunk + 1) < 64 ? N_all - 64 * (chunk + 1) : 64;
-                rd.issue(S0, q, k, v, alpha, beta, nullptr, u, N1, node0 + 64, false, tid, lane, wave, hg, col);
+                const int N1 = N_all - CN * (chunk + 1) < CN ? N_all - CN * (chunk + 1) : CN;
+                rd.issue(S0, q, k, v, alpha, beta, nullptr, u, N1, node0 + CN, false, tid, lane, wave, hg, col);
             }
         }
 
@@ -1160,12 +1163,12 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // the contraction order of that update (entry p is node l(p), the
         // accumulator row order of U), 16-byte chunks swizzled by row.
         __bf16 *KT = Xh + NP * XS, *KTl = Xl + NP * XS;
-        static_assert(!PRE || D * 64 * 2 <= NP * XS * 2, "K^T fits where Q was staged");
-        auto kt_at = [](int j, int p) { return j * 64 + (((p >> 3) ^ (j & 7)) << 3) + (p & 7); };
+        static_assert(!PRE || D * CN * 2 <= NP * XS * 2, "K^T fits where Q was staged");
+        auto kt_at = [](int j, int p) { return j * CN + (((p >> 3) ^ (j & (CN / 8 - 1))) << 3) + (p & 7); };
         if constexpr (PRE) {
-            const int j = tid >> 1, p0 = 32 * (tid & 1);
+            const int j = tid >> 1, p0 = (CN / 2) * (tid & 1);
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
+            for (int c = 0; c < CN / 16; ++c) {
                 bf16x8 hi, lo;
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
@@ -1432,19 +1435,22 @@ hipError_t launch_commit_verify(const void *S_old, const float *U_prev, const vo
 }
 
 // Chain prefill: every chunk of every unit in one launch, the state kept in
-// registers between chunks (see treewy_chain_prefill).
+// registers between chunks (see treewy_chain_prefill).  bf16 tokens run in
+// 32-token chunks: the 32-row kernel has the registers to fetch the next
+// chunk during the current one, and its solve is short.  fp32 tokens run in
+// 64-token chunks at one workgroup per CU, also fetching ahead.
 hipError_t launch_prefill(const void *S0, const void *q, const void *k, const void *v, const float *alpha,
                           const float *beta, int T, int B, int H, bool f32_in, bool bf16_state, void *S_T, void *o,
                           int32_t *err, hipStream_t stream) {
     CommitArgs cm = {};
     cm.S_new = S_T;
     if (bf16_state)
-        return launch<64, false, false, true, CHAIN_PREFILL>(S0, q, k, v, alpha, beta, nullptr, T, T, 0, B, H, o, nullptr,
+        return launch<32, false, false, true, CHAIN_PREFILL>(S0, q, k, v, alpha, beta, nullptr, T, T, 0, B, H, o, nullptr,
                                                    err, cm, stream);
     if (f32_in)
         return launch<64, true, false, false, CHAIN_PREFILL>(S0, q, k, v, alpha, beta, nullptr, T, T, 0, B, H, o, nullptr,
                                                    err, cm, stream);
-    return launch<64, false, false, false, CHAIN_PREFILL>(S0, q, k, v, alpha, beta, nullptr, T, T, 0, B, H, o, nullptr, err,
+    return launch<32, false, false, false, CHAIN_PREFILL>(S0, q, k, v, alpha, beta, nullptr, T, T, 0, B, H, o, nullptr, err,
                                                 cm, stream);
 }
 

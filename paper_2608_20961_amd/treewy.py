@@ -275,8 +275,9 @@ def treewy_accept_greedy(parent, draft_token, target_token, root_token, L_max: i
 
 def treewy_chain_prefill(S0, q, k, v, alpha, beta, S_T=None, o=None, err=None, stream=None
                          ) -> Tuple[torch.Tensor, torch.Tensor]:
-    """Gated delta rule over a chain of T tokens per unit (chunks of 64, one
-    launch): returns the final state and every token's output."""
+    """Gated delta rule over a chain of T tokens per unit (chunks of 32 tokens,
+    64 with fp32 tokens; one launch): returns the final state and every
+    token's output."""
     B, H, T, dk = q.shape
     dv = v.shape[-1]
     dt = q.dtype

@@ -59,7 +59,7 @@ def run(tw, T, dtype, state="f32", in_place=False, seed=0):
     return S0_d, S_T, o
 
 
-@pytest.mark.parametrize("T", [1, 5, 63, 64, 65, 128, 200])
+@pytest.mark.parametrize("T", [1, 5, 31, 32, 33, 63, 64, 65, 128, 200])
 def test_prefill_bf16(tw, T):
     run(tw, T, "bf16")
 
@@ -69,7 +69,7 @@ def test_prefill_f32(tw, T):
     run(tw, T, "f32")
 
 
-@pytest.mark.parametrize("T", [40, 129])
+@pytest.mark.parametrize("T", [32, 40, 129])
 def test_prefill_bf16_state(tw, T):
     run(tw, T, "bf16", state="bf16")
 
@@ -81,8 +81,9 @@ def test_prefill_in_place_and_empty(tw):
 
 
 def test_prefill_equals_verify_then_commit(tw):
-    """One chunk of prefill is a chain verify plus a commit of the whole chain."""
-    T = 48
+    """One chunk of prefill (32 bf16 tokens) is a chain verify plus a commit of
+    the whole chain."""
+    T = 32
     w = chain_workload(T, "bf16", B=3, H=2)
     x = wl.make_inputs(w, seed=9, cfg_key=790)
     S0 = torch.from_numpy(warm_state(w, np.arange(w.units), 9, 791).reshape(w.B, w.H, 128, 128)).to(DEV)
@@ -128,7 +129,7 @@ def test_prefill_many_units_per_workgroup(tw):
 
 
 def test_prefill_bench_length(tw):
-    """The benchmark's chunk count: T = 1024 (sixteen 64-token chunks), 512
+    """The benchmark's chunk count: T = 1024 (thirty-two 32-token chunks), 512
     units, bf16 tokens and an fp32 state; sampled units against the oracle."""
     T, B, H = 1024, 8, 64
     w = wl.Workload("prefill", B, H, T, 128, 128, "bf16", "chain", T, (1,), (0.85, 0.999), (0.05, 0.95), 16,
