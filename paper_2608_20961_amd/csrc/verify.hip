@@ -484,14 +484,28 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // decay and ancestors (gm_all / ge_all, anc_all), so the lane takes
         // them over at once; ext holds the ancestor words of the earlier chunks.
         if (wave == 0) {
-            int ptr = lane < N ? ((!PRE && parent) ? rd.par : lane - 1) : -1;   // (no parent array: a chain)
+            float pm = lane < N ? DecayX::mant(rd.al) : 0.f;
+            int pe = lane < N ? DecayX::expo(rd.al) : 0;
+            uint64_t ext[XT ? MASK_WORDS : 1] = {};
+            uint64_t mask;
+            if constexpr (PRE) {
+                // A chain: node t's ancestors are 0 .. t - 1, and pointer
+                // jumping is the inclusive prefix product below (the same
+                // factors combined in the same order), one shuffle pair per
+                // stride.
+#pragma unroll
+                for (int off = 1; off < NP; off <<= 1) {
+                    const float ym = __shfl_up(pm, off);
+                    const int ye = __shfl_up(pe, off);
+                    if (lane >= off && lane < N) DecayX::mul(pm, pe, ym, ye);
+                }
+                mask = lane < N ? (1ull << lane) - 1ull : 0ull;
+            } else {
+            int ptr = lane < N ? (parent ? rd.par : lane - 1) : -1;   // (no parent array: a chain)
             if (lane < N && (ptr < -1 || ptr >= base + lane)) {
                 flag_error(err, b, TREEWY_FLAG_BAD_PARENT);
                 ptr = -1;
             }
-            float pm = lane < N ? DecayX::mant(rd.al) : 0.f;
-            int pe = lane < N ? DecayX::expo(rd.al) : 0;
-            uint64_t ext[XT ? MASK_WORDS : 1] = {};
             if constexpr (XT) {
                 if (ptr >= 0 && ptr < base) {
                     DecayX::mul(pm, pe, gm_all[ptr], ge_all[ptr]);
@@ -503,7 +517,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                     ptr -= base;
                 }
             }
-            uint64_t mask = ptr >= 0 ? (1ull << ptr) : 0ull;
+            mask = ptr >= 0 ? (1ull << ptr) : 0ull;
             while (__any(ptr >= 0)) {
                 const int src = ptr >= 0 ? ptr : lane;
                 const float pm_s = __shfl(pm, src);
@@ -522,6 +536,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 #pragma unroll
                         for (int j = 0; j < MASK_WORDS; ++j) ext[j] |= ext_s[j];
                 }
+            }
             }
             if (lane < NP) {
                 gm_s[lane] = pm;
