@@ -2,8 +2,8 @@
 
 The reference is eq. 1 run over the chain: every token's output o_t = S_t q_t
 (the oracle's tree routine on a chain of T nodes) and the state after the last
-token (its chain routine).  Chunks of 64 tokens with ragged tails, fp32 and
-bf16 inputs, fp32 and bf16 state, in place.
+token (its chain routine).  Chunks of 32 bf16 tokens (64 fp32 tokens) with
+ragged tails, fp32 and bf16 inputs, fp32 and bf16 state, in place.
 """
 import numpy as np
 import pytest
