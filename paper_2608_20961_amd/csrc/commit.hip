@@ -146,10 +146,8 @@ __global__ __launch_bounds__(THREADS) void commit_kernel(
     for (int i = 0; i < NCH; ++i) {
         uint4 out;
         if constexpr (SBF) {
-            bf16x8 h;
-#pragma unroll
-            for (int e = 0; e < CH; ++e) h[e] = (__bf16)x[i][e];
-            out = __builtin_bit_cast(uint4, h);
+            static_assert(CH == 8, "a bf16 state chunk is one 16-byte store");
+            out = __builtin_bit_cast(uint4, round8(x[i]));
         } else {
             out = __builtin_bit_cast(uint4, f32x4{x[i][0], x[i][1], x[i][2], x[i][3]});
         }

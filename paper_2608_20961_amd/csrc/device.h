@@ -30,21 +30,38 @@ __device__ __forceinline__ f32x16 mma(bf16x8 a, bf16x8 b, f32x16 c) {
 // Row of the 32x32 accumulator tile held in element r by lanes of group hg.
 __device__ __forceinline__ int acc_row(int r, int hg) { return 8 * (r >> 2) + 4 * hg + (r & 3); }
 
+// Two floats -> a packed bf16 pair (element 0 in the low half), both rounded
+// to nearest even by one conversion instruction.  (Element-wise casts became
+// one conversion per element, at half the vector ALU's rate.)
+__device__ __forceinline__ uint32_t pack_bf2(float a, float b) {
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2{a, b}), bf16x2));
+}
+
 // fp32 -> bf16 pair with x ~= hi + lo (|x - hi - lo| <= 2^-16 |x|); both round to nearest even.
+// Per pair of elements: hi by one conversion, each hi widened back to fp32 by a
+// shift or a mask, lo = x - hi (exact), lo by one conversion.
 __device__ __forceinline__ void split8(const float *x, bf16x8 &hi, bf16x8 &lo) {
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    u32x4 h, l;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        __bf16 h = (__bf16)x[e];
-        hi[e] = h;
-        lo[e] = (__bf16)(x[e] - (float)h);
+    for (int p = 0; p < 4; ++p) {
+        const uint32_t hb = pack_bf2(x[2 * p], x[2 * p + 1]);
+        const float h0 = __builtin_bit_cast(float, hb << 16), h1 = __builtin_bit_cast(float, hb & 0xffff0000u);
+        h[p] = hb;
+        l[p] = pack_bf2(x[2 * p] - h0, x[2 * p + 1] - h1);
     }
+    hi = __builtin_bit_cast(bf16x8, h);
+    lo = __builtin_bit_cast(bf16x8, l);
 }
 
 __device__ __forceinline__ bf16x8 round8(const float *x) {
-    bf16x8 h;
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    u32x4 h;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) h[e] = (__bf16)x[e];
-    return h;
+    for (int p = 0; p < 4; ++p) h[p] = pack_bf2(x[2 * p], x[2 * p + 1]);
+    return __builtin_bit_cast(bf16x8, h);
 }
 
 // Raw buffer view of `bytes` bytes at `base` (the descriptor lives in SGPRs).
@@ -134,10 +151,7 @@ __device__ __forceinline__ f32x4 bf4_to_f32(uint2 x) {
     return f32x4{(float)h[0], (float)h[1], (float)h[2], (float)h[3]};
 }
 __device__ __forceinline__ uint2 f32_to_bf4(f32x4 x) {
-    bf16x4 h;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) h[e] = (__bf16)x[e];
-    return __builtin_bit_cast(uint2, h);
+    return uint2{pack_bf2(x[0], x[1]), pack_bf2(x[2], x[3])};
 }
 
 // Cumulative decays in extended range.  g_t, a product of up to 256 gates in

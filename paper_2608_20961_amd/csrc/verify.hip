@@ -563,14 +563,15 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 *reinterpret_cast<uint2 *>(xh + r * XS + Reads::kperm(c + 4)) = make_uint2(val.z, val.w);
             } else {
                 const f32x4 f = *reinterpret_cast<const f32x4 *>(&val);
-                bf16x4 hi, lo;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    hi[e] = (__bf16)f[e];
-                    lo[e] = (__bf16)(f[e] - (float)hi[e]);
-                }
-                *reinterpret_cast<bf16x4 *>(xh + r * XS + Reads::kperm(c)) = hi;
-                *reinterpret_cast<bf16x4 *>(xl + r * XS + Reads::kperm(c)) = lo;
+                uint2 hi, lo;
+                hi.x = pack_bf2(f[0], f[1]);
+                hi.y = pack_bf2(f[2], f[3]);
+                lo.x = pack_bf2(f[0] - __builtin_bit_cast(float, hi.x << 16),
+                                f[1] - __builtin_bit_cast(float, hi.x & 0xffff0000u));
+                lo.y = pack_bf2(f[2] - __builtin_bit_cast(float, hi.y << 16),
+                                f[3] - __builtin_bit_cast(float, hi.y & 0xffff0000u));
+                *reinterpret_cast<uint2 *>(xh + r * XS + Reads::kperm(c)) = hi;
+                *reinterpret_cast<uint2 *>(xl + r * XS + Reads::kperm(c)) = lo;
             }
         };
 #pragma unroll
