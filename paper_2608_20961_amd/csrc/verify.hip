@@ -1298,18 +1298,27 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // neighbouring waves (rows of padding nodes fall past the descriptor).
         constexpr bool O_DIRECT = U_DIRECT || PRE;
         if constexpr (O_DIRECT && !F32IN) {
+            // (rows r and r + 1 rounded by one conversion, stored as two halves)
 #pragma unroll
             for (int m = 0; m < MT; ++m)
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, (__bf16)accp[MT + m][r]), ro,
+                for (int r = 0; r < 16; r += 2) {
+                    const uint32_t pr = pack_bf2(accp[MT + m][r], accp[MT + m][r + 1]);
+                    __builtin_amdgcn_raw_buffer_store_b16((unsigned short)pr, ro,
                                                           ((32 * m + acc_row(r, hg)) * D + col) * 2, 0, CACHED);
+                    __builtin_amdgcn_raw_buffer_store_b16((unsigned short)(pr >> 16), ro,
+                                                          ((32 * m + acc_row(r + 1, hg)) * D + col) * 2, 0, CACHED);
+                }
         } else if constexpr (!F32IN) {
             __syncthreads();                             // o is staged over T: every wave is done with U = T R
 #pragma unroll
             for (int m = 0; m < MT; ++m)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) Os[(32 * m + acc_row(r, hg)) * OS + col] = (__bf16)accp[MT + m][r];
+                for (int r = 0; r < 16; r += 2) {
+                    const uint32_t pr = pack_bf2(accp[MT + m][r], accp[MT + m][r + 1]);
+                    Os[(32 * m + acc_row(r, hg)) * OS + col] = __builtin_bit_cast(__bf16, (unsigned short)pr);
+                    Os[(32 * m + acc_row(r + 1, hg)) * OS + col] = __builtin_bit_cast(__bf16, (unsigned short)(pr >> 16));
+                }
             __syncthreads();
             // (chain prefill: an opaque copy of tid.  These offsets repeat the
             // staging's row / column split, and the compiler would otherwise
