@@ -128,7 +128,11 @@ struct UnitReads {
     static constexpr int KQN = 2 * NP * CPR / THREADS;  // K/Q chunks per thread
     static constexpr int KN = KQN / 2;                  // the first KN are K, the rest Q
     static constexpr int ROW = D * (int)sizeof(In);     // bytes per q/k/v row
-    int par;                                            // wave 0, node = lane
+    // The wave that reads the gates and walks the tree: wave 0, except in
+    // the chain prefill with 32-token chunks, where wave 2 walks each next
+    // chunk while it waits for the solve (see the kernel).
+    static constexpr int WALK_WAVE = CHAIN && NP == 32 ? 2 : 0;
+    int par;                                            // walking wave, node = lane
     float al, be;
     uint4 kq[KQN];                                      // chunk i: row (tid / CPR + i THREADS / CPR) mod NP
     // S0 row `col`, d_k 16s + 8h + 4hg + [0, 4): four floats, or four bf16 in a uint2 for a bf16 state
@@ -180,7 +184,7 @@ struct UnitReads {
                                           const float *alpha, const float *beta, const int32_t *prow,
                                           int u, int N, size_t node0, bool load_state, int tid,
                                           int lane, int wave, int hg, int col) {
-        if (wave == 0) {                                // prow: this unit's parents of the N nodes (null: a chain)
+        if (wave == WALK_WAVE) {                        // prow: this unit's parents of the N nodes (null: a chain)
             // (read unconditionally, an empty descriptor giving 0 for a chain,
             // whose parents the walk takes as lane - 1: a branch here would
             // make the compiler wait for every outstanding memory operation.
@@ -384,6 +388,28 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // keeps the state in registers from one chunk to the next).
         // Otherwise one pass.
         const int chunks = MODE != ONE_PASS ? (N_all + CN - 1) / CN : 1;
+        // A chain's cumulative decays over its n tokens from the gates in
+        // rd.al: node t's ancestors are 0 .. t - 1, and pointer jumping is
+        // the inclusive prefix product below (the same factors combined in
+        // the same order), one shuffle pair per stride.
+        auto chain_decays = [&](int n, float &pm, int &pe) {
+            const int ln = threadIdx.x & 63;
+            pm = ln < n ? DecayX::mant(rd.al) : 0.f;
+            pe = ln < n ? DecayX::expo(rd.al) : 0;
+#pragma unroll
+            for (int off = 1; off < NP; off <<= 1) {
+                const float ym = __shfl_up(pm, off);
+                const int ye = __shfl_up(pe, off);
+                if (ln >= off && ln < n) DecayX::mul(pm, pe, ym, ye);
+            }
+        };
+        // 32-token chunks: wave 2 walks chunk c + 1 during chunk c, in phase
+        // 3, where it would wait for the solve, instead of wave 0 walking
+        // each chunk at its start while the other waves wait at the staging
+        // barrier.
+        constexpr bool WALK_AHEAD = PRE && Reads::WALK_WAVE == 2;
+        float next_pm = 0.f;
+        int next_pe = 0;
         for (int chunk = 0; chunk < chunks; ++chunk) {
         // Lane indices are re-derived each pass from an opaque copy so the
         // per-lane offsets below are recomputed here instead of being hoisted
@@ -455,6 +481,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // The chain prefill fetches the next chunk early where the registers
         // allow: fp32 tokens (one workgroup per CU) and 32-token chunks.
         constexpr bool AHEAD = PRE && (F32IN || NP == 32);
+        static_assert(!WALK_AHEAD || AHEAD, "the next chunk's gates are fetched during this one");
         // The chunked modes read S0 with the first chunk only and keep it in
         // registers (tree chunks use it unchanged in every chunk).
         if constexpr (FUSE) {
@@ -483,24 +510,22 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // Tree chunks: a parent in an earlier chunk already has its final
         // decay and ancestors (gm_all / ge_all, anc_all), so the lane takes
         // them over at once; ext holds the ancestor words of the earlier chunks.
-        if (wave == 0) {
-            float pm = lane < N ? DecayX::mant(rd.al) : 0.f;
-            int pe = lane < N ? DecayX::expo(rd.al) : 0;
+        if (wave == Reads::WALK_WAVE) {
+            float pm;
+            int pe;
             uint64_t ext[XT ? MASK_WORDS : 1] = {};
             uint64_t mask;
             if constexpr (PRE) {
-                // A chain: node t's ancestors are 0 .. t - 1, and pointer
-                // jumping is the inclusive prefix product below (the same
-                // factors combined in the same order), one shuffle pair per
-                // stride.
-#pragma unroll
-                for (int off = 1; off < NP; off <<= 1) {
-                    const float ym = __shfl_up(pm, off);
-                    const int ye = __shfl_up(pe, off);
-                    if (lane >= off && lane < N) DecayX::mul(pm, pe, ym, ye);
+                if (WALK_AHEAD && chunk > 0) {          // walked during the previous chunk
+                    pm = next_pm;
+                    pe = next_pe;
+                } else {
+                    chain_decays(N, pm, pe);
                 }
                 mask = lane < N ? (1ull << lane) - 1ull : 0ull;
             } else {
+            pm = lane < N ? DecayX::mant(rd.al) : 0.f;
+            pe = lane < N ? DecayX::expo(rd.al) : 0;
             int ptr = lane < N ? (parent ? rd.par : lane - 1) : -1;   // (no parent array: a chain)
             if (lane < N && (ptr < -1 || ptr >= base + lane)) {
                 flag_error(err, b, TREEWY_FLAG_BAD_PARENT);
@@ -807,12 +832,13 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             // One tile: its two products on waves 0 and 1; waves 2 and 3 run
             // their share of P meanwhile (wave 3 builds T after the barrier,
             // while waves 0 and 1 run theirs).
-            if (wave == 0)
+            if (wave == 0) {
                 gram_tile(0, 0, Yes{}, No{});
-            else if (wave == 1)
+            } else if (wave == 1) {
                 gram_tile(0, 0, No{}, Yes{});
-            else
+            } else {
                 run_p();
+            }
         } else if (wave < NPAIRS) {
             gram_tile(wave == 0 ? 0 : 1, wave == 2 ? 1 : 0, Yes{}, Yes{});
         } else if (MT == 2 && wave == 3) {
@@ -993,6 +1019,12 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 
         // ---- phase 3: P (see run_p), for the waves that have not run it yet
         if (!EARLY_P || wave < 2) run_p();
+        if constexpr (WALK_AHEAD) {                     // (its gates were issued with the next chunk's reads)
+            if (wave == Reads::WALK_WAVE && chunk + 1 < chunks) {
+                const int n1 = N_all - CN * (chunk + 1) < CN ? N_all - CN * (chunk + 1) : CN;
+                chain_decays(n1, next_pm, next_pe);
+            }
+        }
         __builtin_amdgcn_s_setprio(0);                  // (wave 3 after a deep solve)
         __syncthreads();
 
