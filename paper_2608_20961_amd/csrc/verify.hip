@@ -794,34 +794,50 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 }
             }
             const int ci = 32 * nt + l32;
-            const float inv_mi = 1.f / gm_s[ci];
-            const int ei = ge_s[ci];
             // The accumulator rows come in runs of four consecutive nodes, so
             // their decays, betas and ancestor masks arrive as 16-byte LDS
-            // broadcasts; bit ci of a mask sits in word nt of the row's u64.
+            // broadcasts; bit ci of a mask sits in word nt of the row's u64
+            // (a chain's masks are known: the ancestors of t < N are 0 .. t - 1).
+            // Every read is issued before the first entry is formed.
+            const float gmi = gm_s[ci];
+            const int ei = ge_s[ci];
+            f32x4 g4[4], b4[4];
+            int4 e4[4];
+            uint4 m01[4], m23[4];
 #pragma unroll
-            for (int r4 = 0; r4 < 16; r4 += 4) {
-                const int t0 = 32 * mt + acc_row(r4, hg);      // rows t0 .. t0 + 3
-                const f32x4 g4 = *reinterpret_cast<const f32x4 *>(gm_s + t0);
-                const int4 e4 = *reinterpret_cast<const int4 *>(ge_s + t0);
-                const uint4 m01 = *reinterpret_cast<const uint4 *>(anc_s + t0);
-                const uint4 m23 = *reinterpret_cast<const uint4 *>(anc_s + t0 + 2);
-                const uint32_t w[4] = {nt ? m01.y : m01.x, nt ? m01.w : m01.z,
-                                       nt ? m23.y : m23.x, nt ? m23.w : m23.z};
-                f32x4 b4 = {};
-                if constexpr (WK) b4 = *reinterpret_cast<const f32x4 *>(be_s + t0);
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int t0 = 32 * mt + acc_row(4 * q4, hg);  // rows t0 .. t0 + 3
+                g4[q4] = *reinterpret_cast<const f32x4 *>(gm_s + t0);
+                e4[q4] = *reinterpret_cast<const int4 *>(ge_s + t0);
+                if constexpr (!PRE) {
+                    m01[q4] = *reinterpret_cast<const uint4 *>(anc_s + t0);
+                    m23[q4] = *reinterpret_cast<const uint4 *>(anc_s + t0 + 2);
+                }
+                if constexpr (WK) b4[q4] = *reinterpret_cast<const f32x4 *>(be_s + t0);
+            }
+            const float inv_mi = 1.f / gmi;
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int t0 = 32 * mt + acc_row(4 * q4, hg);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const int r = r4 + e, t = t0 + e;
-                    const bool strict = (w[e] >> l32) & 1u;
-                    const int et = e == 0 ? e4.x : e == 1 ? e4.y : e == 2 ? e4.z : e4.w;
+                    const int r = 4 * q4 + e, t = t0 + e;
+                    bool strict;
+                    if constexpr (PRE) {
+                        strict = ci < t && t < N;
+                    } else {
+                        const uint32_t w = e == 0 ? (nt ? m01[q4].y : m01[q4].x) : e == 1 ? (nt ? m01[q4].w : m01[q4].z)
+                                         : e == 2 ? (nt ? m23[q4].y : m23[q4].x) : (nt ? m23[q4].w : m23[q4].z);
+                        strict = (w >> l32) & 1u;
+                    }
+                    const int et = e == 0 ? e4[q4].x : e == 1 ? e4[q4].y : e == 2 ? e4[q4].z : e4[q4].w;
                     // (the ratio is formed for every entry and then selected:
                     // left to the compiler, the selection became a branch per
                     // entry that waited on its own LDS read)
-                    float rs = DecayX::ratio(g4[e], et, inv_mi, ei);
+                    float rs = DecayX::ratio(g4[q4][e], et, inv_mi, ei);
                     asm volatile("" : "+v"(rs));
                     const float ratio = strict ? rs : (ci == t ? 1.f : 0.f);
-                    if constexpr (WK) Bm[t * MS + ci] = strict ? b4[e] * ratio * gkk[r] : 0.f;
+                    if constexpr (WK) Bm[t * MS + ci] = strict ? b4[q4][e] * ratio * gkk[r] : 0.f;
                     if constexpr (WQ) Am[t * MS + ci] = ratio * gqk[r];
                 }
             }
