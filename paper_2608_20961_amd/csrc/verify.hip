@@ -501,7 +501,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         }
 
         // ---- phase 1: ancestors and cumulative decay by pointer jumping ----
-        // Lane t of wave 0 keeps (ptr, prod, mask): ptr an ancestor of t (or
+        // Lane t of the walking wave keeps (ptr, prod, mask): ptr an ancestor of t (or
         // -1), prod the product of alpha over the path (ptr, t] (in extended
         // range, DecayX: mantissa pm, exponent pe), mask the ancestors of t
         // strictly below t down to and including ptr.  Each round doubles the
