@@ -138,6 +138,33 @@ __device__ __forceinline__ void quad_transpose(f32x4 (&x)[4], int lane) {
     quad_swap<2, 0x4E>(x[1], x[3], lane);
 }
 
+// OR of a 32-bit value over the 64 lanes of a wave, returned wave-uniform:
+// within each row of 16 lanes by DPP (two quad permutations, half-row and
+// row mirrors), then row 0's total into row 1 and row 2's into row 3
+// (row_bcast:15), rows 0-1 into rows 2-3 (row_bcast:31); lane 63 ends with all.
+__device__ __forceinline__ uint32_t wave_or32(uint32_t v) {
+    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);    // quad_perm [1, 0, 3, 2]
+    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);    // quad_perm [2, 3, 0, 1]
+    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false);   // row_half_mirror
+    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false);   // row_mirror
+    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);   // row_bcast:15
+    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);   // row_bcast:31
+    return __builtin_amdgcn_readlane(v, 63);
+}
+__device__ __forceinline__ uint64_t wave_or64(uint64_t v) {
+    return (uint64_t)wave_or32((uint32_t)v) | ((uint64_t)wave_or32((uint32_t)(v >> 32)) << 32);
+}
+
+// The set bits of a wave-uniform word w, compacted: lane c (c < popcount(w))
+// receives the position of the c-th set bit, lowest first.  Lane p, whose bit
+// is set, sends p to lane rank(p) (one LDS-free permute); the lanes of clear
+// bits all send to lane 63, so lanes at or past the count hold no position.
+__device__ __forceinline__ int compact_bits(uint64_t w, int lane) {
+    const bool set = (w >> lane) & 1ull;
+    const int rank = __popcll(w & ((1ull << lane) - 1ull));
+    return __builtin_amdgcn_ds_permute((set ? rank : 63) * 4, lane);
+}
+
 // A copy of x the compiler cannot see through (keeps derived values inside a loop).
 __device__ __forceinline__ int opaque(int x) {
     asm volatile("" : "+v"(x));

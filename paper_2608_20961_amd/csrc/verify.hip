@@ -1091,93 +1091,87 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             float *Ck = reinterpret_cast<float *>(lds), *Cq = Ck + NP * MS;
             static_assert(2 * NP * MS * 4 <= L::B_OFF, "the coupling blocks fit where K/Q were staged");
             for (int j = 0; j < chunk; ++j) {            // uniform loop
-                // This wave's columns of U_j, for the product, issued before
-                // the barriers so that they arrive during them.
-                float ub[4][8];
-                auto load_u = [&]() {
-                    const rsrc_t ruj = make_rsrc(U + ((size_t)u * u_stride + 64 * j) * D, 64 * D * 4);
-#pragma unroll
-                    for (int s = 0; s < 4; ++s)
-#pragma unroll
-                        for (int e = 0; e < 8; ++e) ub[s][e] = ld_f32(ruj, ((16 * s + 8 * hg + e) * D + col) * 4);
-                };
-                {
-                    const int mt = wave >> 1, nt = wave & 1;  // one 32 x 32 tile of the cross gram per wave
-                    // descriptors bounded to the chunks' rows (uniform), the row in the lane's offset
-                    const size_t row0 = (size_t)u * in_stride;
-                    const rsrc_t rak = make_rsrc(k + (row0 + base) * D, N * Reads::ROW);
-                    const rsrc_t raq = make_rsrc(q + (row0 + base) * D, N * Reads::ROW);
-                    const rsrc_t rbk = make_rsrc(k + (row0 + 64 * j) * D, 64 * Reads::ROW);
-                    const int arow = (32 * mt + l32) * Reads::ROW, brow = (32 * nt + l32) * Reads::ROW;
-                    f32x16 gkk = {}, gqk = {};
-                    if (j == 0) {
-                        // This chunk's K and Q are still staged in LDS (in the
-                        // kperm order of d_k): read them there, and the rows of
-                        // chunk 0 in the same order, element e of step s being
-                        // d_k = 16 s + 8 (e / 4) + 4 hg + e % 4.
-                        const __bf16 *xk = Xh + (32 * mt + l32) * XS + 8 * hg, *xq = xk + NP * XS;
+                // Chunk j's nodes with a descendant in this chunk, one bit each
+                // (past the chunk's last node the ancestor words are zero).  In
+                // DFS order these are the ancestors of this chunk's first node,
+                // at most its depth.  The coupling runs over those columns only,
+                // gathered, 32 at a time: usually one group, so half the cross
+                // gram, the U_j reads and the product of all 64 columns, and
+                // none of chunk j's other rows read again.
+                const uint64_t need = wave_or64(anc_all[(base + lane) * MASK_WORDS + j]);
+                const int nneed = __popcll(need);
+                const int my_node = compact_bits(need, lane);   // lane c < nneed: node of chunk j in slot c
+                const int kind = wave & 1, mt = wave >> 1;       // wave: (K or Q rows) x (32-row tile)
+                constexpr int OOB = 1 << 30;                     // past every descriptor: reads zero
+                const size_t row0 = (size_t)u * in_stride;
+                const rsrc_t ra = make_rsrc((kind ? q : k) + (row0 + base) * D, N * Reads::ROW);
+                const rsrc_t rbk = make_rsrc(k + (row0 + 64 * j) * D, 64 * Reads::ROW);
+                const rsrc_t ruj = make_rsrc(U + ((size_t)u * u_stride + 64 * j) * D, 64 * D * 4);
+                for (int g0 = 0; g0 < nneed; g0 += 32) {          // uniform loop
+                    // (lane indices re-derived inside the loop: offsets formed
+                    // from them stay in it instead of being hoisted, and held,
+                    // across the coupling)
+                    const int lane = opaque(threadIdx.x) & 63, l32 = lane & 31, hg = lane >> 5, col = wave * 32 + l32;
+                    const int node_c = __shfl(my_node, g0 + l32);   // this lane's column
+                    const bool live_c = g0 + l32 < nneed;
+                    const int arow = (32 * mt + l32) * Reads::ROW, brow = live_c ? node_c * Reads::ROW : OOB;
+                    f32x16 gx = {};
+                    if (j == 0 && g0 == 0) {
+                        // This chunk's K or Q still staged in LDS (kperm order
+                        // of d_k): read it there, and chunk 0's rows in the
+                        // same order, element e of step s being d_k = 16 s +
+                        // 8 (e / 4) + 4 hg + e % 4.
+                        const __bf16 *xa = Xh + ((kind ? NP : 0) + 32 * mt + l32) * XS + 8 * hg;
                         constexpr int XU = SBF ? 2 : 4;  // steps in flight (a bf16 state has fewer registers to spare)
 #pragma unroll XU
                         for (int s = 0; s < 8; ++s) {
                             const int o0 = (16 * s + 4 * hg) * (int)sizeof(In), o1 = o0 + 8 * (int)sizeof(In);
-                            const bf16x8 ah_k = *reinterpret_cast<const bf16x8 *>(xk + 16 * s);
-                            const bf16x8 ah_q = *reinterpret_cast<const bf16x8 *>(xq + 16 * s);
+                            const bf16x8 ah = *reinterpret_cast<const bf16x8 *>(xa + 16 * s);
                             if constexpr (F32IN) {
-                                const bf16x8 al_k = *reinterpret_cast<const bf16x8 *>(xk + 16 * s + (Xl - Xh));
-                                const bf16x8 al_q = *reinterpret_cast<const bf16x8 *>(xq + 16 * s + (Xl - Xh));
+                                const bf16x8 al = *reinterpret_cast<const bf16x8 *>(xa + 16 * s + (Xl - Xh));
                                 float x8[8];
                                 *reinterpret_cast<f32x4 *>(x8) = ld_f32x4<CACHED>(rbk, brow + o0);
                                 *reinterpret_cast<f32x4 *>(x8 + 4) = ld_f32x4<CACHED>(rbk, brow + o1);
                                 bf16x8 bh, bl;
                                 split8(x8, bh, bl);
-                                gkk = mma(ah_k, bh, gkk);
-                                gkk = mma(ah_k, bl, gkk);
-                                gkk = mma(al_k, bh, gkk);
-                                gqk = mma(ah_q, bh, gqk);
-                                gqk = mma(ah_q, bl, gqk);
-                                gqk = mma(al_q, bh, gqk);
+                                gx = mma(ah, bh, gx);
+                                gx = mma(ah, bl, gx);
+                                gx = mma(al, bh, gx);
                             } else {
                                 const uint2 b0 = ld_u32x2<CACHED>(rbk, brow + o0), b1 = ld_u32x2<CACHED>(rbk, brow + o1);
-                                const bf16x8 b_k = __builtin_bit_cast(bf16x8, make_uint4(b0.x, b0.y, b1.x, b1.y));
-                                gkk = mma(ah_k, b_k, gkk);
-                                gqk = mma(ah_q, b_k, gqk);
+                                gx = mma(ah, __builtin_bit_cast(bf16x8, make_uint4(b0.x, b0.y, b1.x, b1.y)), gx);
                             }
                         }
                     } else {
+                        // (this chunk's rows from the cache: the staging area
+                        // holds the coupling blocks by now)
 #pragma unroll 2
-                    for (int s = 0; s < 8; ++s) {
-                        const int off = (16 * s + 8 * hg) * (int)sizeof(In);
-                        if constexpr (F32IN) {
-                            float x8[3][8];
-                            bf16x8 h[3], l[3];
-                            const rsrc_t rr[3] = {rak, raq, rbk};
-                            const int ro[3] = {arow, arow, brow};
-#pragma unroll
-                            for (int o3 = 0; o3 < 3; ++o3) {
-                                *reinterpret_cast<f32x4 *>(x8[o3]) = ld_f32x4<CACHED>(rr[o3], ro[o3] + off);
-                                *reinterpret_cast<f32x4 *>(x8[o3] + 4) = ld_f32x4<CACHED>(rr[o3], ro[o3] + off + 16);
-                                split8(x8[o3], h[o3], l[o3]);
+                        for (int s = 0; s < 8; ++s) {
+                            const int off = (16 * s + 8 * hg) * (int)sizeof(In);
+                            if constexpr (F32IN) {
+                                float xa8[8], xb8[8];
+                                *reinterpret_cast<f32x4 *>(xa8) = ld_f32x4<CACHED>(ra, arow + off);
+                                *reinterpret_cast<f32x4 *>(xa8 + 4) = ld_f32x4<CACHED>(ra, arow + off + 16);
+                                *reinterpret_cast<f32x4 *>(xb8) = ld_f32x4<CACHED>(rbk, brow + off);
+                                *reinterpret_cast<f32x4 *>(xb8 + 4) = ld_f32x4<CACHED>(rbk, brow + off + 16);
+                                bf16x8 ah, al, bh, bl;
+                                split8(xa8, ah, al);
+                                split8(xb8, bh, bl);
+                                gx = mma(ah, bh, gx);
+                                gx = mma(ah, bl, gx);
+                                gx = mma(al, bh, gx);
+                            } else {
+                                const bf16x8 a8 = __builtin_bit_cast(bf16x8, ld_u32x4<CACHED>(ra, arow + off));
+                                const bf16x8 b8 = __builtin_bit_cast(bf16x8, ld_u32x4<CACHED>(rbk, brow + off));
+                                gx = mma(a8, b8, gx);
                             }
-                            gkk = mma(h[0], h[2], gkk);
-                            gkk = mma(h[0], l[2], gkk);
-                            gkk = mma(l[0], h[2], gkk);
-                            gqk = mma(h[1], h[2], gqk);
-                            gqk = mma(h[1], l[2], gqk);
-                            gqk = mma(l[1], h[2], gqk);
-                        } else {
-                            const bf16x8 a_k = __builtin_bit_cast(bf16x8, ld_u32x4<CACHED>(rak, arow + off));
-                            const bf16x8 a_q = __builtin_bit_cast(bf16x8, ld_u32x4<CACHED>(raq, arow + off));
-                            const bf16x8 b_k = __builtin_bit_cast(bf16x8, ld_u32x4<CACHED>(rbk, brow + off));
-                            gkk = mma(a_k, b_k, gkk);
-                            gqk = mma(a_q, b_k, gqk);
                         }
                     }
-                    }
-                    load_u();
-                    if (j == 0) __syncthreads();         // the coupling blocks are written over the staged K/Q
-                    const int i = 32 * nt + l32;
-                    const float inv_mi = 1.f / gm_all[64 * j + i];  // every node of an earlier chunk is real
-                    const int ei = ge_all[64 * j + i];
+                    __syncthreads();                     // the coupling blocks are written over the staged K/Q (or the last group's)
+                    const int ni = live_c ? node_c : 0;
+                    const float inv_mi = 1.f / gm_all[64 * j + ni];  // every node of an earlier chunk is real
+                    const int ei = ge_all[64 * j + ni];
+                    float *Cw = kind ? Cq : Ck;
                     // (rows in runs of four, one 16-byte read of their decays
                     // each; the barrier keeps the reads from being hoisted)
 #pragma unroll
@@ -1189,35 +1183,49 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 #pragma unroll
                         for (int e = 0; e < 4; ++e) {
                             const int r = r4 + e, t = t0 + e;
-                            const bool a = (anc_all[(base + t) * MASK_WORDS + j] >> i) & 1ull;
+                            const bool a = live_c && ((anc_all[(base + t) * MASK_WORDS + j] >> ni) & 1ull);
                             const int et = e == 0 ? e4.x : e == 1 ? e4.y : e == 2 ? e4.z : e4.w;
                             float ratio = DecayX::ratio(m4[e], et, inv_mi, ei);
                             asm volatile("" : "+v"(ratio));      // (selected below, not branched on)
-                            Ck[t * MS + i] = a ? -b4[e] * ratio * gkk[r] : 0.f;
-                            Cq[t * MS + i] = a ? gqk[r] * ratio : 0.f;
+                            const float val = kind ? gx[r] * ratio : -b4[e] * ratio * gx[r];
+                            Cw[t * MS + l32] = a ? val : 0.f;
                         }
                         __builtin_amdgcn_sched_barrier(0);
                     }
-                }
-                __syncthreads();
+                    // This wave's columns of the gathered U_j rows, in the
+                    // product's slot order.  (Issued here rather than before
+                    // the barriers: each row offset takes a register of its
+                    // own, and held across the epilogue they pushed the
+                    // kernel past its register budget.)
+                    float ub[2][8];
 #pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    bf16x8 bh, bl;
-                    split8(ub[s], bh, bl);
+                    for (int s = 0; s < 2; ++s)
 #pragma unroll
-                    for (int m = 0; m < 2 * MT; ++m) {
-                        const float *crow = (m < MT ? Ck : Cq) + (32 * (m % MT) + l32) * MS + 16 * s + 8 * hg;
-                        float c8[8];
-                        *reinterpret_cast<f32x4 *>(c8) = *reinterpret_cast<const f32x4 *>(crow);
-                        *reinterpret_cast<f32x4 *>(c8 + 4) = *reinterpret_cast<const f32x4 *>(crow + 4);
-                        bf16x8 ah, alo;
-                        split8(c8, ah, alo);
-                        accp[m] = mma(ah, bh, accp[m]);
-                        accp[m] = mma(ah, bl, accp[m]);
-                        accp[m] = mma(alo, bh, accp[m]);
+                        for (int e = 0; e < 8; ++e) {
+                            const int sl = g0 + 16 * s + 8 * hg + e;
+                            const int nd = __shfl(my_node, sl & 63);
+                            ub[s][e] = ld_f32(ruj, sl < nneed ? (nd * D + col) * 4 : OOB);
+                        }
+                    __syncthreads();
+#pragma unroll
+                    for (int s = 0; s < 2; ++s) {
+                        bf16x8 bh, bl;
+                        split8(ub[s], bh, bl);
+#pragma unroll
+                        for (int m = 0; m < 2 * MT; ++m) {
+                            const float *crow = (m < MT ? Ck : Cq) + (32 * (m % MT) + l32) * MS + 16 * s + 8 * hg;
+                            float c8[8];
+                            *reinterpret_cast<f32x4 *>(c8) = *reinterpret_cast<const f32x4 *>(crow);
+                            *reinterpret_cast<f32x4 *>(c8 + 4) = *reinterpret_cast<const f32x4 *>(crow + 4);
+                            bf16x8 ah, alo;
+                            split8(c8, ah, alo);
+                            accp[m] = mma(ah, bh, accp[m]);
+                            accp[m] = mma(ah, bl, accp[m]);
+                            accp[m] = mma(alo, bh, accp[m]);
+                        }
                     }
                 }
-                __syncthreads();                         // the coupling blocks are rewritten next
+                __syncthreads();                         // the coupling blocks are rewritten next (or U staged there)
             }
         }
 
