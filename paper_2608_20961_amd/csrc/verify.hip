@@ -94,6 +94,14 @@ struct VerifyLds {
     static constexpr bool V_IN_BA = V_BYTES <= 2 * M_BYTES;  // V staged over B and A before the gram
     static constexpr int V_OFF = V_IN_BA ? B_OFF : END_O;
     static constexpr int BASE_BYTES = V_IN_BA ? END_O : END_O + V_BYTES;
+    // Chain prefill of 32-token chunks: T and A also as bf16 hi / lo planes
+    // (rows of TS, columns in the kperm order of the products that read
+    // them), split once by the wave that forms them instead of by every wave
+    // that reads them.
+    static constexpr int TS = NP + 8;                   // bf16 per plane row (16-byte aligned rows)
+    static constexpr int PLANE_BYTES = NP * TS * 2;
+    static constexpr int TP_OFF = BASE_BYTES;           // T hi, T lo, A hi, A lo
+    static constexpr int PRE_BYTES = TP_OFF + 4 * PLANE_BYTES;
     // Fused commit: the accepted path (node, weight, then its length and g_a),
     // and CL path rows at a time, transposed: k as [d_k][CL], w U as [d_v][CL].
     static constexpr int CL = 8;
@@ -310,11 +318,15 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
     constexpr int XS = L::XS, MS = L::MS, US = L::US, OS = L::OS;
     constexpr int CHUNK = Reads::CHUNK, CPR = Reads::CPR, KQN = Reads::KQN;
 
-    __shared__ __attribute__((aligned(16))) unsigned char lds[XT ? L::TREE_BYTES : L::BYTES];
+    __shared__ __attribute__((aligned(16))) unsigned char lds[XT ? L::TREE_BYTES : PRE && NP == 32 ? L::PRE_BYTES : L::BYTES];
     __bf16 *Xh = reinterpret_cast<__bf16 *>(lds);
     __bf16 *Xl = reinterpret_cast<__bf16 *>(lds + L::XLO_OFF);
     float *Bm = reinterpret_cast<float *>(lds + L::B_OFF);
     float *Am = reinterpret_cast<float *>(lds + L::A_OFF);
+    // (chain prefill of 32-token chunks: T and A as bf16 planes)
+    constexpr bool PLANES = PRE && NP == 32;
+    __bf16 *Thi = reinterpret_cast<__bf16 *>(lds + L::TP_OFF), *Tlo = Thi + NP * L::TS;
+    __bf16 *Ahi = Tlo + NP * L::TS, *Alo = Ahi + NP * L::TS;
     float *Us = reinterpret_cast<float *>(lds);          // U is staged where K/Q were, after P
     __bf16 *Os = reinterpret_cast<__bf16 *>(lds + L::O_OFF);   // o staging (bf16 input only)
     float *be_s = reinterpret_cast<float *>(lds + L::BETA_OFF);
@@ -816,6 +828,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 if constexpr (WK) b4[q4] = *reinterpret_cast<const f32x4 *>(be_s + t0);
             }
             const float inv_mi = 1.f / gmi;
+            float av[16];                                // (planes: A's column ci, split below)
 #pragma unroll
             for (int q4 = 0; q4 < 4; ++q4) {
                 const int t0 = 32 * mt + acc_row(4 * q4, hg);
@@ -838,7 +851,33 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                     asm volatile("" : "+v"(rs));
                     const float ratio = strict ? rs : (ci == t ? 1.f : 0.f);
                     if constexpr (WK) Bm[t * MS + ci] = strict ? b4[q4][e] * ratio * gkk[r] : 0.f;
-                    if constexpr (WQ) Am[t * MS + ci] = ratio * gqk[r];
+                    if constexpr (WQ) {
+                        if constexpr (PLANES) {
+                            // (rounded to fp32 here, as stored in A elsewhere: the
+                            // split below must not fuse this product into its lo)
+                            av[r] = ratio * gqk[r];
+                            asm("" : "+v"(av[r]));
+                        }
+                        else {
+                            Am[t * MS + ci] = ratio * gqk[r];
+                        }
+                    }
+                }
+            }
+            if constexpr (WQ && PLANES) {
+                // rows t and t + 1 (accumulator entries r, r + 1) split by one
+                // conversion pair, written at column kperm(ci) of both planes
+                const int pc = Reads::kperm(ci);
+#pragma unroll
+                for (int r = 0; r < 16; r += 2) {
+                    const int t = 32 * mt + acc_row(r, hg);
+                    const uint32_t hb = pack_bf2(av[r], av[r + 1]);
+                    const uint32_t lb = pack_bf2(av[r] - __builtin_bit_cast(float, hb << 16),
+                                                 av[r + 1] - __builtin_bit_cast(float, hb & 0xffff0000u));
+                    Ahi[t * L::TS + pc] = __builtin_bit_cast(__bf16, (unsigned short)hb);
+                    Ahi[(t + 1) * L::TS + pc] = __builtin_bit_cast(__bf16, (unsigned short)(hb >> 16));
+                    Alo[t * L::TS + pc] = __builtin_bit_cast(__bf16, (unsigned short)lb);
+                    Alo[(t + 1) * L::TS + pc] = __builtin_bit_cast(__bf16, (unsigned short)(lb >> 16));
                 }
             }
         };
@@ -1030,6 +1069,33 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 const f32x16 tt = block_product(B10 + l32 * MS + 32, B10 + l32, Two{});       // T11 M
 #pragma unroll
                 for (int r2 = 0; r2 < 16; ++r2) B10[acc_row(r2, hg) * MS + l32] = -tt[r2];
+            }
+        }
+
+        // Chain prefill of 32-token chunks: wave 3 splits T into its bf16
+        // planes once (lane: row lane % 32, columns 16 (lane / 32) .. + 15,
+        // written in kperm order), after either solve has written T over B.
+        if constexpr (PLANES) {
+            if (wave == 3) {
+                const int row = lane & 31, c0 = 16 * (lane >> 5);
+                f32x4 g[4];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) g[c] = *reinterpret_cast<const f32x4 *>(Bm + row * MS + c0 + 4 * c);
+                float x8[2][8];                          // kperm within 16 columns: groups 0, 2, then 1, 3
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    x8[0][e] = g[0][e];
+                    x8[0][4 + e] = g[2][e];
+                    x8[1][e] = g[1][e];
+                    x8[1][4 + e] = g[3][e];
+                }
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    bf16x8 th, tl;
+                    split8(x8[h], th, tl);
+                    *reinterpret_cast<bf16x8 *>(Thi + row * L::TS + c0 + 8 * h) = th;
+                    *reinterpret_cast<bf16x8 *>(Tlo + row * L::TS + c0 + 8 * h) = tl;
+                }
             }
         }
 
@@ -1282,12 +1348,17 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
                 if (s > 2 * mt + 1) continue;            // T is zero above the diagonal blocks
-                const float *trow = Tsrc + (32 * mt + l32) * MS + 32 * m + 16 * hh + 4 * hg;
-                float ta[8];
-                *reinterpret_cast<f32x4 *>(ta) = *reinterpret_cast<const f32x4 *>(trow);
-                *reinterpret_cast<f32x4 *>(ta + 4) = *reinterpret_cast<const f32x4 *>(trow + 8);
                 bf16x8 ah, alo;
-                split8(ta, ah, alo);
+                if constexpr (PLANES) {                  // (split once, into the planes)
+                    ah = *reinterpret_cast<const bf16x8 *>(Thi + l32 * L::TS + 16 * hh + 8 * hg);
+                    alo = *reinterpret_cast<const bf16x8 *>(Tlo + l32 * L::TS + 16 * hh + 8 * hg);
+                } else {
+                    const float *trow = Tsrc + (32 * mt + l32) * MS + 32 * m + 16 * hh + 4 * hg;
+                    float ta[8];
+                    *reinterpret_cast<f32x4 *>(ta) = *reinterpret_cast<const f32x4 *>(trow);
+                    *reinterpret_cast<f32x4 *>(ta + 4) = *reinterpret_cast<const f32x4 *>(trow + 8);
+                    split8(ta, ah, alo);
+                }
                 accv[mt] = mma(ah, bh, accv[mt]);
                 accv[mt] = mma(ah, bl, accv[mt]);
                 accv[mt] = mma(alo, bh, accv[mt]);
@@ -1336,12 +1407,17 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
                 if (s > 2 * mt + 1) continue;
-                const float *arow = Am + (32 * mt + l32) * MS + 32 * m + 16 * hh + 4 * hg;
-                float aa[8];
-                *reinterpret_cast<f32x4 *>(aa) = *reinterpret_cast<const f32x4 *>(arow);
-                *reinterpret_cast<f32x4 *>(aa + 4) = *reinterpret_cast<const f32x4 *>(arow + 8);
                 bf16x8 ah, alo;
-                split8(aa, ah, alo);
+                if constexpr (PLANES) {                  // (split once, into the planes)
+                    ah = *reinterpret_cast<const bf16x8 *>(Ahi + l32 * L::TS + 16 * hh + 8 * hg);
+                    alo = *reinterpret_cast<const bf16x8 *>(Alo + l32 * L::TS + 16 * hh + 8 * hg);
+                } else {
+                    const float *arow = Am + (32 * mt + l32) * MS + 32 * m + 16 * hh + 4 * hg;
+                    float aa[8];
+                    *reinterpret_cast<f32x4 *>(aa) = *reinterpret_cast<const f32x4 *>(arow);
+                    *reinterpret_cast<f32x4 *>(aa + 4) = *reinterpret_cast<const f32x4 *>(arow + 8);
+                    split8(aa, ah, alo);
+                }
                 accp[MT + mt] = mma(ah, bh, accp[MT + mt]);
                 accp[MT + mt] = mma(ah, bl, accp[MT + mt]);
                 accp[MT + mt] = mma(alo, bh, accp[MT + mt]);
