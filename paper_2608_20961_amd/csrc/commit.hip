@@ -21,7 +21,7 @@ namespace treewy {
 constexpr int MAX_PATH = MAX_TREE;
 constexpr int STAGE_ROWS = 64;                           // path rows staged per pass
 
-template <bool F32K, bool SBF>
+template <bool F32K, bool SBF, bool SCALAR_PATH>
 __global__ __launch_bounds__(THREADS) void commit_kernel(
     const void *S0, const float *__restrict__ U, const void *__restrict__ k_,
     const float *__restrict__ alpha, const int32_t *__restrict__ path,
@@ -54,22 +54,61 @@ __global__ __launch_bounds__(THREADS) void commit_kernel(
     // order and (with a parent array) is its child, entry 0 a child of the
     // committed prefix.  A bad path commits nothing.
     const int len_in = path_len[b];
-    const bool len_ok = len_in >= 0 && len_in <= L_max;
-    if (tid == 0) s_bad = len_ok ? 0 : 1;
-    __syncthreads();
-    if (len_ok)
-        for (int l = tid; l < len_in; l += THREADS) {
-            const int a = path[(size_t)b * L_max + l];
-            const int prev = l > 0 ? path[(size_t)b * L_max + l - 1] : -1;
-            if (a < 0 || a >= N || a <= prev || (parent && parent[(size_t)b * N + a] != prev)) {
-                s_bad = 1;
-            } else {
-                s_node[l] = a;
-                s_al[l] = alpha[node0 + a];
+    bool ok = len_in >= 0 && len_in <= L_max;
+    if constexpr (SCALAR_PATH) {
+        // Every wave checks the whole path on wave-uniform scalar loads,
+        // eight entries at a time.  Those count apart from the state's vector
+        // reads in flight, so the check need not wait for the state (vector
+        // loads return in order).  Used where a workgroup has few units, so
+        // that each unit's latency shows.
+        if (ok) {
+            int prev = -1;
+            for (int l0 = 0; l0 < len_in; l0 += 8) {     // uniform loop
+                int a[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) a[e] = l0 + e < len_in ? path[(size_t)b * L_max + l0 + e] : -1;
+                float al[8];
+                int pa[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const bool in_range = l0 + e < len_in && a[e] >= 0 && a[e] < N;
+                    al[e] = in_range ? alpha[node0 + a[e]] : 1.f;
+                    pa[e] = in_range && parent ? parent[(size_t)b * N + a[e]] : prev;
+                }
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    if (l0 + e < len_in) {
+                        if (a[e] < 0 || a[e] >= N || a[e] <= prev || (parent && pa[e] != prev)) ok = false;
+                        prev = a[e];
+                        if (tid == e) {
+                            s_node[l0 + e] = a[e];
+                            s_al[l0 + e] = al[e];
+                        }
+                    }
+                }
             }
         }
-    __syncthreads();
-    const bool ok = s_bad == 0;
+        __syncthreads();
+    } else {
+        // One entry per thread (the path loads wait for the state's reads,
+        // which other workgroups' streams hide when a workgroup walks many
+        // units).
+        if (tid == 0) s_bad = ok ? 0 : 1;
+        __syncthreads();
+        if (ok)
+            for (int l = tid; l < len_in; l += THREADS) {
+                const int a = path[(size_t)b * L_max + l];
+                const int prev = l > 0 ? path[(size_t)b * L_max + l - 1] : -1;
+                if (a < 0 || a >= N || a <= prev || (parent && parent[(size_t)b * N + a] != prev)) {
+                    s_bad = 1;
+                } else {
+                    s_node[l] = a;
+                    s_al[l] = alpha[node0 + a];
+                }
+            }
+        __syncthreads();
+        ok = s_bad == 0;
+    }
     const int len = ok ? len_in : 0;
     // w_l = product of alpha over the entries after l, and g_a = the product
     // over all: lane i of wave 0 holds entries 4i .. 4i + 3.
@@ -179,10 +218,18 @@ hipError_t launch_commit(const void *S0, const float *U, const void *k, const fl
         const long long g = (long long)cus * per_cu;
         return dim3((unsigned)(units < g ? units : g));
     };
-#define TREEWY_COMMIT(F, S)                                                                                   \
-    hipLaunchKernelGGL((commit_kernel<F, S>), grid_of(reinterpret_cast<const void *>(&commit_kernel<F, S>)),    \
-                       dim3(THREADS), lds, stream, S0, U, k, alpha, path, path_len, L_max, parent, N, H, S_new, err, \
-                       units)
+    // The path check on scalar loads (see the kernel) where a workgroup has
+    // at most four units; one entry per thread where it walks more.
+#define TREEWY_COMMIT(F, S)                                                                                      \
+    do {                                                                                                         \
+        const dim3 grid = grid_of(reinterpret_cast<const void *>(&commit_kernel<F, S, false>));                  \
+        if (units <= 4 * (long long)grid.x)                                                                      \
+            hipLaunchKernelGGL((commit_kernel<F, S, true>), grid, dim3(THREADS), lds, stream, S0, U, k, alpha, path, \
+                               path_len, L_max, parent, N, H, S_new, err, units);                                 \
+        else                                                                                                     \
+            hipLaunchKernelGGL((commit_kernel<F, S, false>), grid, dim3(THREADS), lds, stream, S0, U, k, alpha, path, \
+                               path_len, L_max, parent, N, H, S_new, err, units);                                 \
+    } while (0)
     if (f32_k) {
         if (bf16_state) TREEWY_COMMIT(true, true);
         else TREEWY_COMMIT(true, false);
