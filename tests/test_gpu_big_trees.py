@@ -88,6 +88,29 @@ def test_fixed_width_trees(tw, widths):
     check(tw, Case(w, seed=6, cfg_key=1400 + N, inputs=x), "widths %s (N=%d)" % (widths, N))
 
 
+def test_coupling_groups(tw):
+    """128-node trees whose second chunk descends from exactly m nodes of the
+    first (m = 40, 32, 33 across the sequences: a chain of m nodes, the rest
+    of the first chunk leaves on it, the second chunk hanging off all m), so
+    the coupling gathers one full group, one and a half, and a second group
+    of a single column."""
+    N = 128
+    w = tree_workload(N, 42, B=3, H=2, caps=(9,))
+    x = wl.make_inputs(w, seed=8, cfg_key=1500)
+    rng = np.random.default_rng(15)
+    for b, m in enumerate((40, 32, 33)):
+        par = np.empty(N, dtype=np.int32)
+        par[:m] = np.arange(-1, m - 1)
+        par[m:64] = (np.arange(m, 64) - m) % m
+        par[64:] = (np.arange(64, N) - 64) % m
+        x["parent"][b] = par
+        nodes = wl.ancestors_and_self(par, int(rng.integers(64, N)))
+        x["path"][b] = -1
+        x["path"][b, :len(nodes)] = nodes
+        x["path_len"][b] = len(nodes)
+    check(tw, Case(w, seed=8, cfg_key=1500, inputs=x), "coupling groups (m = 40, 32, 33)")
+
+
 def test_full_size_sampled(tw):
     """The 397B layer shape with 128-node trees: the launch the benchmark times."""
     w = wl.BIG_TREE
