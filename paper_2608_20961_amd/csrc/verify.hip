@@ -20,11 +20,9 @@
 // dense column sweep for deep ones).  U = T R
 // and A U then run on the matrix cores with R and U taken straight from the
 // accumulator registers (the contraction index is permuted to match the
-// accumulator layout; T and A are read in the same permuted order).  U
-// leaves straight from its accumulators (each store instruction writes whole
-// 128-byte lines) at 64 nodes in one pass, else through LDS; so does bf16 O
-// at 64 nodes in one pass and in the chain prefill (half lines, merged in
-// L2), else through LDS as whole-row 16-byte stores.
+// accumulator layout; T and A are read in the same permuted order).  U and
+// O leave straight from their accumulators: each U store instruction writes
+// whole 128-byte lines, each bf16 O store half lines, merged in L2.
 //
 // Streaming.  All of a unit's HBM reads are issued at once, in the order they
 // are consumed (tree and gates, K/Q, V, then S0), through buffer descriptors
@@ -74,8 +72,6 @@ template <int NP, bool F32IN, bool FUSE = false>
 struct VerifyLds {
     static constexpr int XS = D + 8;                    // bf16 per staged K/Q row (pad breaks bank aliasing)
     static constexpr int MS = NP + 4;                   // floats per row of the N x N matrices
-    static constexpr int US = D + 4;                    // floats per staged U row
-    static constexpr int OS = D + 8;                    // bf16 per staged o row
     static constexpr int X_BYTES = 2 * NP * XS * 2;     // [K; Q] in bf16
     static constexpr int XLO_OFF = X_BYTES;             // low halves of fp32 K/Q
     static constexpr int B_OFF = X_BYTES * (F32IN ? 2 : 1);
@@ -85,15 +81,12 @@ struct VerifyLds {
     static constexpr int G_OFF = BETA_OFF + NP * 4;     // cumulative decays: mantissas ...
     static constexpr int GE_OFF = G_OFF + NP * 4;       // ... and exponents (see DecayX)
     static constexpr int ANC_OFF = GE_OFF + NP * 4;
-    static constexpr int FLAG_OFF = ANC_OFF + NP * 8;   // 1 when every node has <= FAST ancestors
+    static constexpr int FLAG_OFF = ANC_OFF + NP * 8;   // depth class of the chunk (see phase 3a)
     static constexpr int END = FLAG_OFF + 16;
-    static constexpr bool O_IN_B = NP * OS * 2 <= M_BYTES;   // o staged where B was, else appended
-    static constexpr int O_OFF = O_IN_B ? B_OFF : END;
-    static constexpr int END_O = (O_IN_B || F32IN) ? END : END + NP * OS * 2;
     static constexpr int V_BYTES = NP * D * (F32IN ? 4 : 2);
     static constexpr bool V_IN_BA = V_BYTES <= 2 * M_BYTES;  // V staged over B and A before the gram
-    static constexpr int V_OFF = V_IN_BA ? B_OFF : END_O;
-    static constexpr int BASE_BYTES = V_IN_BA ? END_O : END_O + V_BYTES;
+    static constexpr int V_OFF = V_IN_BA ? B_OFF : END;
+    static constexpr int BASE_BYTES = V_IN_BA ? END : END + V_BYTES;
     // Chain prefill of 32-token chunks: T and A also as bf16 hi / lo planes
     // (rows of TS, columns in the kperm order of the products that read
     // them), split once by the wave that forms them instead of by every wave
@@ -117,9 +110,8 @@ struct VerifyLds {
     static constexpr int GEALL_OFF = GALL_OFF + MAX_TREE * 4;
     static constexpr int ANCALL_OFF = GEALL_OFF + MAX_TREE * 4;
     static constexpr int TREE_BYTES = ANCALL_OFF + MAX_TREE * MASK_WORDS * 8;
-    static_assert(NP * US * 4 <= B_OFF, "U staging must fit where K/Q were staged");
     static_assert(B_OFF % 16 == 0 && A_OFF % 16 == 0 && BETA_OFF % 16 == 0 && G_OFF % 16 == 0 && GE_OFF % 16 == 0 &&
-                  ANC_OFF % 32 == 0 && O_OFF % 16 == 0 && V_OFF % 16 == 0 &&
+                  ANC_OFF % 32 == 0 && V_OFF % 16 == 0 &&
                   KPT_OFF % 16 == 0 && UWT_OFF % 16 == 0 && ANCALL_OFF % 16 == 0, "alignment");
 };
 
@@ -315,7 +307,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
     using Reads = UnitReads<NP, F32IN, FUSE, SBF, PRE>;
     constexpr int SB = Reads::SB;
     constexpr int MT = NP / 32;                          // 32-row tiles of nodes
-    constexpr int XS = L::XS, MS = L::MS, US = L::US, OS = L::OS;
+    constexpr int XS = L::XS, MS = L::MS;
     constexpr int CHUNK = Reads::CHUNK, CPR = Reads::CPR, KQN = Reads::KQN;
 
     __shared__ __attribute__((aligned(16))) unsigned char lds[XT ? L::TREE_BYTES : PRE && NP == 32 ? L::PRE_BYTES : L::BYTES];
@@ -327,17 +319,16 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
     constexpr bool PLANES = PRE && NP == 32;
     __bf16 *Thi = reinterpret_cast<__bf16 *>(lds + L::TP_OFF), *Tlo = Thi + NP * L::TS;
     __bf16 *Ahi = Tlo + NP * L::TS, *Alo = Ahi + NP * L::TS;
-    float *Us = reinterpret_cast<float *>(lds);          // U is staged where K/Q were, after P
-    __bf16 *Os = reinterpret_cast<__bf16 *>(lds + L::O_OFF);   // o staging (bf16 input only)
     float *be_s = reinterpret_cast<float *>(lds + L::BETA_OFF);
     float *gm_s = reinterpret_cast<float *>(lds + L::G_OFF);  // g_t = gm_s[t] 2^ge_s[t] (DecayX)
     int *ge_s = reinterpret_cast<int *>(lds + L::GE_OFF);
     uint64_t *anc_s = reinterpret_cast<uint64_t *>(lds + L::ANC_OFF);
-    int *shallow_s = reinterpret_cast<int *>(lds + L::FLAG_OFF);
+    int *depth_s = reinterpret_cast<int *>(lds + L::FLAG_OFF);
     float *gm_all = reinterpret_cast<float *>(lds + L::GALL_OFF);           // (tree chunks)
     int *ge_all = reinterpret_cast<int *>(lds + L::GEALL_OFF);
     uint64_t *anc_all = reinterpret_cast<uint64_t *>(lds + L::ANCALL_OFF);
     constexpr int FAST = 8;                              // ancestors a lane holds in registers
+    constexpr int MED = 16;                              // ancestors a lane walks with B read one step ahead
     // fused commit staging (unused otherwise)
     constexpr int CL = L::CL;
     In *KpT = reinterpret_cast<In *>(lds + L::KPT_OFF);
@@ -562,9 +553,10 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 const int ptr_s = __shfl(ptr, src);
                 const uint64_t mask_s = __shfl(mask, src);
                 uint64_t ext_s[XT ? MASK_WORDS : 1] = {};
-                if constexpr (XT)
+                if constexpr (XT)                        // (the words of this and later chunks are zero)
 #pragma unroll
-                    for (int j = 0; j < MASK_WORDS; ++j) ext_s[j] = __shfl(ext[j], src);
+                    for (int j = 0; j < MASK_WORDS; ++j)
+                        if (j < chunk) ext_s[j] = __shfl(ext[j], src);
                 if (ptr >= 0) {
                     DecayX::mul(pm, pe, pm_s, pe_s);
                     mask |= mask_s;
@@ -587,8 +579,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
 #pragma unroll
                 for (int j = 0; j < MASK_WORDS; ++j) anc_all[(base + lane) * MASK_WORDS + j] = j == chunk ? mask : ext[j];
             }
-            const bool shallow = !__any(__popcll(mask) > FAST);
-            if (lane == 0) *shallow_s = shallow ? 1 : 0;
+            const int depth_class = !__any(__popcll(mask) > FAST) ? 1 : !__any(__popcll(mask) > MED) ? 2 : 0;
+            if (lane == 0) *depth_s = depth_class;
         }
         // Fused: the path rows go to LDS.
         if constexpr (FUSE) stage_store(0, cp);
@@ -931,7 +923,8 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 }
             }
         }
-        const bool shallow = *shallow_s != 0;
+        const int depth_class = *depth_s;
+        const bool shallow = depth_class == 1, medium = depth_class == 2;
         // ---- phase 3a: rows of T = (I + B)^{-1}, on wave 3 while the others run P
         // (T (I + B))[t, j] = 0 for j != t gives, walking t's ancestors j from
         // the nearest upwards, T[t, j] = -sum over i in {t} and the ancestors
@@ -974,6 +967,45 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             for (int kk = 0; kk < FAST; ++kk) Tt[a[kk]] = x[kk];   // past m: a zero on the diagonal
             if (t < N) Tt[t] = 1.f;
         }
+        // Trees of at most MED ancestors per node: the same recurrence, with
+        // the entries of B that ancestor kk needs (B[t, a_kk] and B[a_l, a_kk]
+        // for the nearer ancestors l) read one ancestor ahead, as too many to
+        // hold at once.  The reads for ancestor kk + 1 take their column
+        // offset through an empty asm that also takes x[kk - 1], so they are
+        // issued while x[kk] is formed and not hoisted further.
+        if (medium && wave == 3 && lane < NP) {
+            const int t = lane;
+            uint64_t rem = anc_s[t];
+            int a[MED];
+#pragma unroll
+            for (int kk = 0; kk < MED; ++kk) {
+                a[kk] = rem ? 63 - __builtin_clzll(rem) : t;
+                rem &= ~(1ull << (a[kk] & 63));
+            }
+            float x[MED], cur[MED], nxt[MED];
+            cur[0] = Bm[t * MS + a[0]];
+#pragma unroll
+            for (int kk = 0; kk < MED; ++kk) {
+                if (kk + 1 < MED) {
+                    int ak = a[kk + 1];
+                    if (kk > 0) asm volatile("" : "+v"(ak) : "v"(x[kk - 1]));
+                    nxt[0] = Bm[t * MS + ak];
+#pragma unroll
+                    for (int l = 0; l <= kk; ++l) nxt[l + 1] = Bm[a[l] * MS + ak];
+                }
+                float acc = cur[0];
+#pragma unroll
+                for (int l = 0; l < kk; ++l) acc += x[l] * cur[l + 1];
+                x[kk] = -acc;
+#pragma unroll
+                for (int l = 0; l <= kk + 1 && l < MED; ++l) cur[l] = nxt[l];
+            }
+            // (every read of B above precedes these stores)
+            float *Tt = Bm + t * MS;
+#pragma unroll
+            for (int kk = 0; kk < MED; ++kk) Tt[a[kk]] = x[kk];     // past m: a zero on the diagonal
+            if (t < N) Tt[t] = 1.f;
+        }
         // Deeper trees: the same recurrence as a dense column sweep.  Lane t
         // keeps r[j] = sum over the finished columns i of T[t, i] B[i, j]; at
         // column i (from the last down) T[t, i] = -r[i] is final and row i
@@ -987,7 +1019,7 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
         // matrix cores, in place over B10 (M = B10 T00 is parked there first
         // so that one accumulator tile is live at a time).  LDS accesses of
         // one wave complete in order, so no barrier separates the steps.
-        if (!shallow && wave == 3) {
+        if (depth_class == 0 && wave == 3) {
             // (the solve, then at 64 rows this wave's share of P, is the
             // critical path here: the wave goes first at instruction issue on
             // its SIMD until then)
@@ -1374,30 +1406,18 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             wt_s[lane] = lane < N ? DecayX::ratio(gm_s[N - 1], ge_s[N - 1], 1.f / gm_s[lane], ge_s[lane]) : 0.f;
         const rsrc_t ru = make_rsrc(PRE ? nullptr : U + (unode0 + base) * D, PRE ? 0 : N * D * 4);
         const rsrc_t ro = make_rsrc(o + node0 * D, N * D * (int)sizeof(In));
-        // U leaves while A U runs (rows of padding nodes fall past the end of
-        // the descriptor and are dropped).  In one pass, straight from the
-        // accumulators: each store instruction writes the lane group's 32
-        // columns, one whole 128-byte line, of two rows.  In the chunked modes
-        // (where those registers are not to spare) through LDS as whole rows,
-        // 16 bytes per lane.
-        constexpr bool U_DIRECT = MODE == ONE_PASS;
-        if constexpr (U_DIRECT) {
+        // U leaves while A U runs, straight from the accumulators (rows of
+        // padding nodes fall past the end of the descriptor and are dropped):
+        // each store instruction writes the lane group's 32 columns, one whole
+        // 128-byte line, of two rows.  Tree chunks keep U in the cache for the
+        // coupling of later chunks; the chain prefill keeps U in registers for
+        // its state update and stores none.
+        if constexpr (!PRE) {
 #pragma unroll
             for (int m = 0; m < MT; ++m)
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
-                    st_f32<STREAM>(ru, ((32 * m + acc_row(r, hg)) * D + col) * 4, accv[m][r]);
-        } else if constexpr (!PRE) {                     // (the chain prefill keeps U in registers and K in LDS)
-#pragma unroll
-            for (int m = 0; m < MT; ++m)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) Us[(32 * m + acc_row(r, hg)) * US + col] = accv[m][r];
-            __syncthreads();
-#pragma unroll
-            for (int it = 0; it < NP * (D / 4) / THREADS; ++it) {
-                const int idx = tid + THREADS * it, t = idx / (D / 4), c = (idx % (D / 4)) * 4;
-                st_u32x4<XT ? CACHED : STREAM>(ru, (t * D + c) * 4, *reinterpret_cast<const uint4 *>(Us + t * US + c));
-            }
+                    st_f32<XT ? CACHED : STREAM>(ru, ((32 * m + acc_row(r, hg)) * D + col) * 4, accv[m][r]);
         }
 #pragma unroll
         for (int s = 0; s < 2 * MT; ++s) {
@@ -1424,12 +1444,11 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
             }
             __builtin_amdgcn_sched_barrier(0);
         }
-        // In one pass and in the chain prefill, bf16 o straight from the
-        // accumulators as well.  A store instruction writes half a line (32
-        // bf16) of two rows; the default policy lets L2 merge the halves from
-        // neighbouring waves (rows of padding nodes fall past the descriptor).
-        constexpr bool O_DIRECT = U_DIRECT || PRE;
-        if constexpr (O_DIRECT && !F32IN) {
+        // o straight from the accumulators as well.  With bf16 inputs a store
+        // instruction writes half a line (32 bf16) of two rows; the default
+        // policy lets L2 merge the halves from neighbouring waves (rows of
+        // padding nodes fall past the descriptor).
+        if constexpr (!F32IN) {
             // (rows r and r + 1 rounded by one conversion, stored as two halves)
 #pragma unroll
             for (int m = 0; m < MT; ++m)
@@ -1441,26 +1460,6 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                     __builtin_amdgcn_raw_buffer_store_b16((unsigned short)(pr >> 16), ro,
                                                           ((32 * m + acc_row(r + 1, hg)) * D + col) * 2, 0, CACHED);
                 }
-        } else if constexpr (!F32IN) {
-            __syncthreads();                             // o is staged over T: every wave is done with U = T R
-#pragma unroll
-            for (int m = 0; m < MT; ++m)
-#pragma unroll
-                for (int r = 0; r < 16; r += 2) {
-                    const uint32_t pr = pack_bf2(accp[MT + m][r], accp[MT + m][r + 1]);
-                    Os[(32 * m + acc_row(r, hg)) * OS + col] = __builtin_bit_cast(__bf16, (unsigned short)pr);
-                    Os[(32 * m + acc_row(r + 1, hg)) * OS + col] = __builtin_bit_cast(__bf16, (unsigned short)(pr >> 16));
-                }
-            __syncthreads();
-            // (chain prefill: an opaque copy of tid.  These offsets repeat the
-            // staging's row / column split, and the compiler would otherwise
-            // keep those values live across the whole chunk, spilled.)
-            const int tid_o = PRE ? opaque(tid) : tid;
-#pragma unroll
-            for (int it = 0; it < NP * (D / 8) / THREADS; ++it) {
-                const int idx = tid_o + THREADS * it, t = idx / (D / 8), c = (idx % (D / 8)) * 8;
-                st_u32x4<STREAM>(ro, (t * D + c) * 2, *reinterpret_cast<const uint4 *>(Os + t * OS + c));
-            }
         } else {
 #pragma unroll
             for (int m = 0; m < MT; ++m)

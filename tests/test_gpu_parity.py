@@ -79,6 +79,43 @@ def test_long_chains(tw, N):
     run_and_check(tw, Case(w, seed=3, cfg_key=200 + N), "chain N=%d" % N)
 
 
+def spine_tree(N, anc, rng):
+    """A tree whose deepest node has exactly `anc` ancestors: nodes 0..anc
+    form a chain and every later node hangs off a random earlier node of
+    depth below anc."""
+    par = np.full(N, wl.ROOT, dtype=np.int32)
+    depth = np.zeros(N, dtype=np.int64)
+    for t in range(1, N):
+        if t <= anc:
+            par[t] = t - 1
+        elif anc > 0:
+            par[t] = rng.choice(np.flatnonzero(depth[:t] < anc))
+        depth[t] = depth[par[t]] + 1 if par[t] != wl.ROOT else 0
+    assert depth.max() == anc and wl.is_topological(par)
+    return par
+
+
+@pytest.mark.parametrize("N,ancs", [(32, (9, 8, 17)), (32, (16, 0, 31)), (64, (8, 9, 16)), (64, (17, 16, 12))])
+def test_solve_depth_classes(tw, N, ancs):
+    """The three solves of T = (I + B)^{-1}, chosen per unit by its deepest
+    node: at most 8 ancestors (entries of B gathered into registers), 9 to 16
+    (B read one ancestor ahead), more (the dense blocked sweep).  Sequence b
+    has exactly ancs[b] ancestors at its deepest node, so every boundary
+    meets the others within one launch."""
+    w = wl.Workload("spine", len(ancs), 2, N, 128, 128, "bf16", "tree", max(ancs) + 1, (2,), (0.85, 0.999),
+                    (0.05, 0.95), 16, "uniform_node")
+    x = wl.make_inputs(w, seed=11, cfg_key=600 + N)
+    rng = np.random.default_rng(N)
+    for b, anc in enumerate(ancs):
+        par = spine_tree(N, anc, rng)
+        x["parent"][b] = par
+        nodes = wl.ancestors_and_self(par, int(rng.integers(N)))
+        x["path"][b] = -1
+        x["path"][b, :len(nodes)] = nodes
+        x["path_len"][b] = len(nodes)
+    run_and_check(tw, Case(w, seed=11, cfg_key=600 + N, inputs=x), "depth classes N=%d %s" % (N, ancs))
+
+
 def test_fixed_width_tree_shapes(tw):
     for shape in ([2, 1, 1], [3, 3, 3], [4, 3, 3]):
         par = wl.width_tree(shape)
