@@ -204,6 +204,10 @@ struct UnitReads {
         const rsrc_t rv = make_rsrc(vv + node0 * D, N * ROW);
 #pragma unroll
         for (int i = 0; i < VQN; ++i) vq[i] = ld_u32x4<STREAM>(rv, (tid + THREADS * i) * 16);
+        // (the state's reads go last: vector reads return in order, so the
+        // staging of K/Q/V then need not wait for the state.  Left to itself
+        // the scheduler has moved the V reads behind them.)
+        __builtin_amdgcn_sched_barrier(0);
         if (load_state) issue_state(S0, u, hg, col);    // (chain prefill: the state is already in registers)
     }
 
