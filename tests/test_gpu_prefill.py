@@ -3,7 +3,10 @@
 The reference is eq. 1 run over the chain: every token's output o_t = S_t q_t
 (the oracle's tree routine on a chain of T nodes) and the state after the last
 token (its chain routine).  Chunks of 32 bf16 tokens (64 fp32 tokens) with
-ragged tails, fp32 and bf16 inputs, fp32 and bf16 state, in place.
+ragged tails, fp32 and bf16 inputs, fp32 and bf16 state, in place.  The
+lengths put each of the three solves of T = (I + B)^{-1} in the last chunk:
+at most 9 tokens (8 ancestors: registers), 10 to 17 (B read one ancestor
+ahead: 12, 49 = 32 + 17, 10, 81 = 64 + 17, 17) and more (the dense sweep).
 """
 import numpy as np
 import pytest
@@ -59,17 +62,17 @@ def run(tw, T, dtype, state="f32", in_place=False, seed=0):
     return S0_d, S_T, o
 
 
-@pytest.mark.parametrize("T", [1, 5, 31, 32, 33, 63, 64, 65, 128, 200])
+@pytest.mark.parametrize("T", [1, 5, 12, 31, 32, 33, 49, 63, 64, 65, 128, 200])
 def test_prefill_bf16(tw, T):
     run(tw, T, "bf16")
 
 
-@pytest.mark.parametrize("T", [1, 64, 130])
+@pytest.mark.parametrize("T", [1, 10, 64, 81, 130])
 def test_prefill_f32(tw, T):
     run(tw, T, "f32")
 
 
-@pytest.mark.parametrize("T", [32, 40, 129])
+@pytest.mark.parametrize("T", [17, 32, 40, 129])
 def test_prefill_bf16_state(tw, T):
     run(tw, T, "bf16", state="bf16")
 
@@ -80,10 +83,10 @@ def test_prefill_in_place_and_empty(tw):
     assert torch.equal(S_T, S0) and o.numel() == 0
 
 
-def test_prefill_equals_verify_then_commit(tw):
-    """One chunk of prefill (32 bf16 tokens) is a chain verify plus a commit of
-    the whole chain."""
-    T = 32
+@pytest.mark.parametrize("T", [5, 12, 32])
+def test_prefill_equals_verify_then_commit(tw, T):
+    """One chunk of prefill (5, 12 or 32 bf16 tokens: each of the three
+    solves) is a chain verify plus a commit of the whole chain."""
     w = chain_workload(T, "bf16", B=3, H=2)
     x = wl.make_inputs(w, seed=9, cfg_key=790)
     S0 = torch.from_numpy(warm_state(w, np.arange(w.units), 9, 791).reshape(w.B, w.H, 128, 128)).to(DEV)
