@@ -136,6 +136,20 @@ def test_fused_round_sizes_differ(tw, Np, Nc, dtype):
     TwoRounds(mk(Np), mk(Nc), seed=Np + Nc).check_against_oracle(tw, "Np=%d Nc=%d %s" % (Np, Nc, dtype))
 
 
+@pytest.mark.parametrize("kind,Nc,depth", [("chain", 12, 12), ("chain", 17, 17), ("chain", 33, 33), ("chain", 64, 64),
+                                           ("tree", 64, 14)])
+def test_fused_current_round_solves(tw, kind, Nc, depth):
+    """The current round's tree taking each solve of T = (I + B)^{-1} inside
+    the fused call: chains of 12 and 17 and a 64-node tree of depth 14 (B read
+    one ancestor ahead), chains of 33 and 64 (the dense sweep, at 64 rows)."""
+    wp = wl.Workload("fused", 2, 3, 16, 128, 128, "bf16", "tree", 6, (4, 4, 2), (0.85, 0.999), (0.05, 0.95),
+                     16, "uniform_node")
+    order = "chain_depth_0_to_N" if kind == "chain" else "uniform_node"
+    wc = wl.Workload(kind, 2, 3, Nc, 128, 128, "bf16", kind, depth, (1,) if kind == "chain" else (3,),
+                     (0.85, 0.999), (0.05, 0.95), 16, order)
+    TwoRounds(wp, wc, seed=40 + Nc).check_against_oracle(tw, "current %s N=%d depth %d" % (kind, Nc, depth))
+
+
 @pytest.mark.parametrize("L", [9, 17, 40, 64])
 def test_fused_long_paths(tw, L):
     """Accepted paths longer than one staging pass (8 rows) of the rank update."""
