@@ -70,6 +70,16 @@ def test_ragged(tw, N):
     run_case(tw, bf16_case(w, N, 600 + N), "ragged N=%d" % N)
 
 
+@pytest.mark.parametrize("kind,N,depth", [("chain", 12, 12), ("chain", 33, 33), ("chain", 64, 64), ("tree", 64, 14)])
+def test_solves(tw, kind, N, depth):
+    """Trees taking the medium solve (chain of 12, 64-node tree of depth 14)
+    and the dense sweep (chains of 33 and 64) with a bf16 state."""
+    order = "chain_depth_0_to_N" if kind == "chain" else "uniform_node"
+    w = wl.Workload(kind, 2, 3, N, 128, 128, "bf16", kind, depth, (1,) if kind == "chain" else (3,), (0.85, 0.999),
+                    (0.05, 0.95), 16, order)
+    run_case(tw, bf16_case(w, N, 650 + N), "%s N=%d depth %d" % (kind, N, depth))
+
+
 def test_bit_identical_to_fp32_state_with_bf16_values(tw):
     w = wl.scaled(wl.WORKLOADS[3], B=4, H=6)
     case = bf16_case(w, 3, 3)
