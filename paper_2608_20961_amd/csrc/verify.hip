@@ -721,7 +721,13 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                 split8(sv, h, l);
             };
             bf16x8 nbh, nbl;
-            if constexpr (SPLIT_AHEAD) split_state(rd, 0, nbh, nbl);
+            // Tree chunks with an fp32 state: S0 is the same in every chunk, so
+            // the first chunk keeps each step's hi / lo split in the registers
+            // that held it and the later chunks read the split back.
+            constexpr bool KEEP_SPLIT = XT && !SBF;
+            const bool split_now = !KEEP_SPLIT || chunk == 0;   // (uniform)
+            if constexpr (SPLIT_AHEAD)
+                if (split_now) split_state(rd, 0, nbh, nbl);
             f32x16 dcur = {};
 #pragma unroll
             for (int s = 0; s < 8; ++s) {
@@ -746,9 +752,18 @@ __global__ __launch_bounds__(THREADS, (F32IN && NP == 64) ? 1 : 2) void verify_k
                     bh = __builtin_bit_cast(bf16x8, make_uint4(rd.s0[s][0].x, rd.s0[s][0].y, rd.s0[s][1].x,
                                                                rd.s0[s][1].y));
                 } else if constexpr (SPLIT_AHEAD) {
-                    bh = nbh;
-                    bl = nbl;
-                    if (s < 7) split_state(rd, s + 1, nbh, nbl);
+                    if (split_now) {
+                        bh = nbh;
+                        bl = nbl;
+                        if (s < 7) split_state(rd, s + 1, nbh, nbl);
+                        if constexpr (KEEP_SPLIT) {
+                            rd.s0[s][0] = __builtin_bit_cast(f32x4, bh);
+                            rd.s0[s][1] = __builtin_bit_cast(f32x4, bl);
+                        }
+                    } else {
+                        bh = __builtin_bit_cast(bf16x8, rd.s0[s][0]);
+                        bl = __builtin_bit_cast(bf16x8, rd.s0[s][1]);
+                    }
                 } else {
                     split_state(rd, s, bh, bl);
                 }
