@@ -111,6 +111,41 @@ def test_coupling_groups(tw):
     check(tw, Case(w, seed=8, cfg_key=1500, inputs=x), "coupling groups (m = 40, 32, 33)")
 
 
+def mixed_solve_tree(rng):
+    """A 256-node tree whose four chunks take different solves of their
+    diagonal block: a chain of 30 with leaves (dense sweep), segments of 8
+    hanging off earlier nodes (registers), segments of 14 (B read one ancestor
+    ahead), a chain of 40 (dense sweep again)."""
+    N = 256
+    par = np.empty(N, dtype=np.int32)
+    par[:30] = np.arange(-1, 29)
+    par[30:64] = rng.integers(0, 21, 34)
+    for i in range(64):
+        par[64 + i] = rng.integers(0, 64) if i % 8 == 0 else 64 + i - 1
+        par[128 + i] = rng.integers(0, 128) if i % 14 == 0 else 128 + i - 1
+        par[192 + i] = (rng.integers(0, 192) if i == 0 else 192 + i - 1) if i < 40 else 192 + rng.integers(0, 10)
+    assert wl.is_topological(par)
+    return par
+
+
+def test_chunks_with_different_solves(tw):
+    """One unit's chunks take the dense sweep, the register gather, the
+    medium solve and the sweep again, in one launch."""
+    N = 256
+    w = tree_workload(N, 120, B=2, H=3, caps=(9,))
+    x = wl.make_inputs(w, seed=9, cfg_key=1600)
+    rng = np.random.default_rng(16)
+    for b in range(w.B):
+        par = mixed_solve_tree(rng)
+        x["parent"][b] = par
+        nodes = wl.ancestors_and_self(par, int(rng.integers(192, N)))
+        assert len(nodes) <= x["path"].shape[1]
+        x["path"][b] = -1
+        x["path"][b, :len(nodes)] = nodes
+        x["path_len"][b] = len(nodes)
+    check(tw, Case(w, seed=9, cfg_key=1600, inputs=x), "chunks with different solves")
+
+
 def test_full_size_sampled(tw):
     """The 397B layer shape with 128-node trees: the launch the benchmark times."""
     w = wl.BIG_TREE
