@@ -57,26 +57,27 @@ __global__ __launch_bounds__(THREADS) void commit_kernel(
     bool ok = len_in >= 0 && len_in <= L_max;
     if constexpr (SCALAR_PATH) {
         // Every wave checks the whole path on wave-uniform scalar loads,
-        // eight entries at a time.  Those count apart from the state's vector
+        // four entries at a time.  Those count apart from the state's vector
         // reads in flight, so the check need not wait for the state (vector
         // loads return in order).  Used where a workgroup has few units, so
         // that each unit's latency shows.
         if (ok) {
             int prev = -1;
-            for (int l0 = 0; l0 < len_in; l0 += 8) {     // uniform loop
-                int a[8];
+            constexpr int PCH = 4;                       // path entries per pass (at eight, 49 scalar registers spilled)
+            for (int l0 = 0; l0 < len_in; l0 += PCH) {   // uniform loop
+                int a[PCH];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) a[e] = l0 + e < len_in ? path[(size_t)b * L_max + l0 + e] : -1;
-                float al[8];
-                int pa[8];
+                for (int e = 0; e < PCH; ++e) a[e] = l0 + e < len_in ? path[(size_t)b * L_max + l0 + e] : -1;
+                float al[PCH];
+                int pa[PCH];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
+                for (int e = 0; e < PCH; ++e) {
                     const bool in_range = l0 + e < len_in && a[e] >= 0 && a[e] < N;
                     al[e] = in_range ? alpha[node0 + a[e]] : 1.f;
                     pa[e] = in_range && parent ? parent[(size_t)b * N + a[e]] : prev;
                 }
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
+                for (int e = 0; e < PCH; ++e) {
                     if (l0 + e < len_in) {
                         if (a[e] < 0 || a[e] >= N || a[e] <= prev || (parent && pa[e] != prev)) ok = false;
                         prev = a[e];
